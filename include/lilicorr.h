@@ -1,0 +1,141 @@
+/*
+ * lilicorr.h — C ABI of the LiLiCorr draft-correlation hot path on MI355X (gfx950).
+ *
+ * LiLiCorr (Lightweight Likelihood Correlation of Parallel Drafts) turns the per-slot vocabulary
+ * logits of a parallel block drafter into one coherent draft: it keeps the top-K candidates of
+ * every slot (Sec. 3.2), gives each candidate a unit-norm "in" and "out" vector (Sec. 3.2 and the
+ * implementation appendix), scores every adjacent pair with sigma * cos(out, in) (Eq. pair) and
+ * commits the block left to right with a greedy argmax walk (Sec. 3.5), whose local softmax is
+ * Eq. (localar).
+ *
+ * Conventions shared by every call
+ *  - Tensors are caller-owned, device-resident (HBM), contiguous, row-major with the innermost
+ *    dimension last, and 16-byte aligned. bf16 tensors hold raw bfloat16 bit patterns.
+ *  - N requests, B slots per request (every slot carries logits and candidates; the optional
+ *    anchor of the paper, its slot 0, enters only through anchor_out / S0), K candidates per
+ *    slot, V vocabulary size, d width of the in/out vectors.
+ *  - Every call is asynchronous on `stream` (0 = the null stream) and allocates no memory;
+ *    the library keeps no state between calls, so concurrent calls on different streams are safe
+ *    when their outputs do not overlap.
+ *  - Arguments are validated on the host before anything is launched: a negative status means
+ *    nothing was launched and no output was written. LILICORR_ERR_HIP reports a failed launch.
+ *  - Preconditions the library does not check (reading device data would cost a sync): logits
+ *    finite or -inf with at least one finite value per slot; ids inside [0, V). Breaking them
+ *    gives unspecified (but memory-safe) results.
+ *  - Limits: 1 <= K <= min(V, 64); B >= 1; N >= 1; d a multiple of 16 with 16 <= d <= 1024;
+ *    N*B*V < 2^62; V < 2^31.
+ */
+#ifndef LILICORR_H_
+#define LILICORR_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LILICORR_F32 = 0,  /* IEEE binary32 */
+    LILICORR_BF16 = 1, /* bfloat16 bit patterns (uint16) */
+} lilicorr_dtype;
+
+typedef enum {
+    LILICORR_OK = 0,
+    LILICORR_ERR_INVALID_ARG = -1, /* null pointer, size out of range, bad dtype */
+    LILICORR_ERR_UNSUPPORTED = -2, /* a limit above is exceeded */
+    LILICORR_ERR_ALIGNMENT = -3,   /* a pointer is not 16-byte aligned */
+    LILICORR_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
+    LILICORR_ERR_HIP = -5,         /* a kernel launch failed */
+} lilicorr_status;
+
+/*
+ * Step 1 — vocabulary-wide log-normalisation fused with top-K candidate selection.
+ * Sec. 3.2 keeps the drafter's K most probable tokens of every slot as candidates; the paper's
+ * serving path extracts them in the same kernel that normalises the logits over the vocabulary
+ * (implementation appendix, "Serving").
+ *
+ *   logits    [N][B][V] in `dtype` (LILICORR_F32 or LILICORR_BF16), read once.
+ *   ids       [N][B][K] int32 out: token ids ordered by logit descending, ties to the lower id
+ *             (-0 and +0 compare equal).
+ *   logp      [N][B][K] fp32 out: logits[id] - log(sum_v exp(logits[v])).
+ *   workspace device scratch of at least lilicorr_topk_workspace_bytes(N, B, V, K) bytes (may be
+ *             NULL when that is 0); owned by the caller, no initial contents needed, clobbered.
+ */
+size_t lilicorr_topk_workspace_bytes(int64_t N, int64_t B, int64_t V, int K);
+lilicorr_status lilicorr_topk(const void *logits, lilicorr_dtype dtype, int64_t N, int64_t B,
+                              int64_t V, int K, int32_t *ids, float *logp, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Step 2 — candidate in/out vectors. Each candidate carries an out vector and an in vector in
+ * R^d, each normalised to unit L2 norm (Sec. 3.2; the two linear heads of the implementation
+ * appendix). The trained head is out of reach here; its final linear heads are stood in for by
+ * u_in = E[id] W_in and u_out = E[id] W_out (row-vector convention, W[i][j] maps input i to
+ * output j), then v = u / ||u|| (a zero u gives a zero v).
+ *
+ * lilicorr_pack_weights converts W_in, W_out ([d][d] fp32, device) once into the library's
+ * matrix-core layout: each fp32 weight is split exactly into three bf16 terms whose sum is the
+ * fp32 value, so bf16 products accumulate in fp32 to fp32-grade results.
+ *   packed    device buffer of lilicorr_packed_weight_bytes(d) bytes, owned by the caller.
+ *
+ * lilicorr_candidate_vectors
+ *   ids       [N][B][K] int32 (as produced by step 1).
+ *   E         [V][d] embedding table in `e_dtype` (bf16 uses matrix cores; fp32 uses vector FMA).
+ *   packed_w  buffer filled by lilicorr_pack_weights for the same d.
+ *   in_vec, out_vec  [N][B][K][d] fp32 out.
+ */
+size_t lilicorr_packed_weight_bytes(int d);
+lilicorr_status lilicorr_pack_weights(const float *W_in, const float *W_out, int d, void *packed,
+                                      hipStream_t stream);
+lilicorr_status lilicorr_candidate_vectors(const int32_t *ids, const void *E,
+                                           lilicorr_dtype e_dtype, int64_t V, int d,
+                                           const void *packed_w, int64_t N, int64_t B, int K,
+                                           float *in_vec, float *out_vec, hipStream_t stream);
+
+/*
+ * Step 3 — batched pair matching scores, Eq. (pair): phi(s, k, k') = sigma * cos(out_{s,k},
+ * in_{s+1,k'}); one K x K matrix per adjacent slot pair, batched over the block (Sec. 3.5).
+ *
+ *   in_vec, out_vec  [N][B][K][d] fp32 (need not be normalised: the cosine normalises).
+ *   anchor_out       [N][d] fp32 or NULL: the anchor's out vector (K_0 = 1 in Eq. pair).
+ *   sigma            fixed cosine scale (8.0 in the paper's hyper-parameter table).
+ *   S                [N][B-1][K][K] fp32 out: S[n][t][k][k'] = sigma*cos(out[n][t][k], in[n][t+1][k']).
+ *                    May be NULL when B == 1.
+ *   S0               [N][K] fp32 out, required iff anchor_out != NULL:
+ *                    S0[n][k'] = sigma*cos(anchor_out[n], in[n][0][k']).
+ * A cosine with a zero vector is 0.
+ */
+lilicorr_status lilicorr_pair_scores(const float *in_vec, const float *out_vec,
+                                     const float *anchor_out, int64_t N, int64_t B, int K, int d,
+                                     float sigma, float *S, float *S0, hipStream_t stream);
+
+/*
+ * Step 4 — greedy left-to-right walk (Sec. 3.5) and the local log-likelihood of Eq. (localar).
+ * For every request n, slot t = 0..B-1:
+ *   z_t[k] = P_t[k] + logp_weight * logp[n][t][k]   (one fp32 rounding; logp_weight = 0 is the
+ *            paper's rule), with P_0 = S0[n] (all zeros when S0 is NULL) and
+ *            P_t = S[n][t-1][c_{t-1}] for t >= 1,
+ *   c_t    = the lowest k attaining max_k z_t[k],
+ *   draft[n][t] = ids[n][t][c_t], choice[n][t] = c_t, logq[n][t] = z_t[c_t] - log sum_k exp z_t[k].
+ *
+ *   S       [N][B-1][K][K] fp32 (may be NULL when B == 1); S0 [N][K] fp32 or NULL.
+ *   logp    [N][B][K] fp32 (read only when logp_weight != 0, but must be valid).
+ *   ids     [N][B][K] int32.
+ *   draft   [N][B] int32 out; choice [N][B] int32 out or NULL; logq [N][B] fp32 out or NULL.
+ */
+lilicorr_status lilicorr_greedy_walk(const float *S, const float *S0, const float *logp,
+                                     const int32_t *ids, int64_t N, int64_t B, int K,
+                                     float logp_weight, int32_t *draft, int32_t *choice,
+                                     float *logq, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char *lilicorr_status_string(lilicorr_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LILICORR_H_ */

@@ -217,8 +217,8 @@ int oracle_pair_scores(const float *in_vec, const float *out_vec, const float *a
  * Slot 0 uses the anchor scores S0 (all zero when no anchor is given). Ties go to the lowest k.
  * draft[t] = ids[t][c_t], choice[t] = c_t.
  * The node score z is formed in float with one rounding (fmaf), the precision the GPU kernel
- * takes its argmax in; with lambda = 0 it is the float score itself. logq is then evaluated in
- * double from those float scores.
+ * takes its argmax in; with lambda = 0 (the paper's rule, z = phi alone) the logp term is absent
+ * and z is the float score itself. logq is then evaluated in double from those float scores.
  * ------------------------------------------------------------------------------------------- */
 
 int oracle_greedy_walk(const float *S, const float *S0, const float *logp, const int32_t *ids,
@@ -239,7 +239,8 @@ int oracle_greedy_walk(const float *S, const float *S0, const float *logp, const
                     pair = S0 ? S0[n * K + k] : 0.0f;
                 else
                     pair = S[((n * (B - 1) + (t - 1)) * K + prev) * K + k];
-                z[k] = fmaf(logp_weight, logp[(n * B + t) * K + k], pair);
+                z[k] = (logp_weight == 0.0f) ? pair
+                                              : fmaf(logp_weight, logp[(n * B + t) * K + k], pair);
             }
             int best = 0;
             for (int k = 1; k < K; ++k)

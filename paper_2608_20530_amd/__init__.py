@@ -1,0 +1,222 @@
+"""LiLiCorr draft-correlation hot path on MI355X (gfx950): Python binding of liblilicorr.so.
+
+The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.h):
+
+  lilicorr_topk               logits [N,B,V] -> ids, logp [N,B,K]       (Sec. 3.2; serving appendix)
+  lilicorr_pack_weights       W_in, W_out [d,d] -> matrix-core layout   (once per weight set)
+  lilicorr_candidate_vectors  ids, E -> in_vec, out_vec [N,B,K,d]       (Sec. 3.2 unit-norm heads)
+  lilicorr_pair_scores        in/out -> S [N,B-1,K,K] (+ S0 [N,K])      (Eq. pair)
+  lilicorr_greedy_walk        S, S0, logp, ids -> draft, choice, logq   (Sec. 3.5, Eq. localar)
+
+This module only marshals arguments: torch supplies device memory and the current HIP stream,
+and every step of the path runs in the library's kernels. There is no fallback: if the library
+is missing or fails to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "LIB_PATH", "load_library", "LilicorrError", "SIGMA",
+    "lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
+    "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
+    "lilicorr_greedy_walk", "lilicorr_status_string",
+    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "draft_block",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblilicorr.so")
+SIGMA = 8.0  # cosine scale of Eq. (pair), hyper-parameter table of the implementation appendix
+
+F32, BF16 = 0, 1
+
+_lib = None
+
+
+class LilicorrError(RuntimeError):
+    pass
+
+
+def load_library() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise LilicorrError(f"{LIB_PATH} is not built (run __graft_entry__.build() or "
+                            "python paper_2608_20530_amd/build.py); there is no fallback path")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I, SZ, F = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t,
+                        ctypes.c_float)
+    sig = {
+        "lilicorr_topk_workspace_bytes": ([I64, I64, I64, I], SZ),
+        "lilicorr_topk": ([P, I, I64, I64, I64, I, P, P, P, SZ, P], I),
+        "lilicorr_packed_weight_bytes": ([I], SZ),
+        "lilicorr_pack_weights": ([P, P, I, P, P], I),
+        "lilicorr_candidate_vectors": ([P, P, I, I64, I, P, I64, I64, I, P, P, P], I),
+        "lilicorr_pair_scores": ([P, P, P, I64, I64, I, I, F, P, P, P], I),
+        "lilicorr_greedy_walk": ([P, P, P, P, I64, I64, I, F, P, P, P, P], I),
+        "lilicorr_status_string": ([I], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+# ---- raw C ABI (same names and argument order as include/lilicorr.h) ----------------------------
+
+def lilicorr_status_string(status: int) -> str:
+    return load_library().lilicorr_status_string(status).decode()
+
+
+def _call(name: str, *args) -> int:
+    rc = getattr(load_library(), name)(*args)
+    if rc != 0:
+        raise LilicorrError(f"{name}: {lilicorr_status_string(rc)} (status {rc})")
+    return rc
+
+
+def lilicorr_topk_workspace_bytes(N: int, B: int, V: int, K: int) -> int:
+    return int(load_library().lilicorr_topk_workspace_bytes(N, B, V, K))
+
+
+def lilicorr_packed_weight_bytes(d: int) -> int:
+    return int(load_library().lilicorr_packed_weight_bytes(d))
+
+
+def lilicorr_topk(logits, dtype, N, B, V, K, ids, logp, workspace, workspace_bytes, stream):
+    return _call("lilicorr_topk", logits, dtype, N, B, V, K, ids, logp, workspace,
+                 workspace_bytes, stream)
+
+
+def lilicorr_pack_weights(W_in, W_out, d, packed, stream):
+    return _call("lilicorr_pack_weights", W_in, W_out, d, packed, stream)
+
+
+def lilicorr_candidate_vectors(ids, E, e_dtype, V, d, packed_w, N, B, K, in_vec, out_vec, stream):
+    return _call("lilicorr_candidate_vectors", ids, E, e_dtype, V, d, packed_w, N, B, K, in_vec,
+                 out_vec, stream)
+
+
+def lilicorr_pair_scores(in_vec, out_vec, anchor_out, N, B, K, d, sigma, S, S0, stream):
+    return _call("lilicorr_pair_scores", in_vec, out_vec, anchor_out, N, B, K, d, sigma, S, S0,
+                 stream)
+
+
+def lilicorr_greedy_walk(S, S0, logp, ids, N, B, K, logp_weight, draft, choice, logq, stream):
+    return _call("lilicorr_greedy_walk", S, S0, logp, ids, N, B, K, logp_weight, draft, choice,
+                 logq, stream)
+
+
+# ---- torch conveniences (marshalling only) -----------------------------------------------------
+
+def _dev(t: torch.Tensor | None, name: str, dtypes=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise LilicorrError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise LilicorrError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise LilicorrError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    return t.data_ptr()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    return BF16 if t.dtype == torch.bfloat16 else F32
+
+
+def topk(logits: torch.Tensor, K: int, *, out=None, workspace=None):
+    """logits [N,B,V] bf16/fp32 -> (ids [N,B,K] int32, logp [N,B,K] fp32)."""
+    N, B, V = logits.shape
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(N, B, K, dtype=torch.int32, device=dev),
+               torch.empty(N, B, K, dtype=torch.float32, device=dev))
+    ids, logp = out
+    need = lilicorr_topk_workspace_bytes(N, B, V, K)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    lilicorr_topk(_dev(logits, "logits", (torch.bfloat16, torch.float32)), _dtype_code(logits),
+                  N, B, V, K, _dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)),
+                  _dev(workspace, "workspace"), workspace.numel(), _stream())
+    return ids, logp
+
+
+def pack_weights(W_in: torch.Tensor, W_out: torch.Tensor, *, out=None) -> torch.Tensor:
+    d = W_in.shape[0]
+    need = lilicorr_packed_weight_bytes(d)
+    packed = out if out is not None else torch.empty(max(need, 16), dtype=torch.uint8, device=W_in.device)
+    lilicorr_pack_weights(_dev(W_in, "W_in", (torch.float32,)), _dev(W_out, "W_out", (torch.float32,)),
+                          d, _dev(packed, "packed"), _stream())
+    return packed
+
+
+def candidate_vectors(ids: torch.Tensor, E: torch.Tensor, packed: torch.Tensor, *, out=None):
+    """ids [N,B,K] int32, E [V,d] bf16/fp32 -> (in_vec, out_vec) [N,B,K,d] fp32."""
+    N, B, K = ids.shape
+    V, d = E.shape
+    if out is None:
+        out = (torch.empty(N, B, K, d, dtype=torch.float32, device=ids.device),
+               torch.empty(N, B, K, d, dtype=torch.float32, device=ids.device))
+    in_vec, out_vec = out
+    lilicorr_candidate_vectors(_dev(ids, "ids", (torch.int32,)),
+                               _dev(E, "E", (torch.bfloat16, torch.float32)), _dtype_code(E), V, d,
+                               _dev(packed, "packed"), N, B, K,
+                               _dev(in_vec, "in_vec", (torch.float32,)),
+                               _dev(out_vec, "out_vec", (torch.float32,)), _stream())
+    return in_vec, out_vec
+
+
+def pair_scores(in_vec: torch.Tensor, out_vec: torch.Tensor, anchor_out=None, sigma: float = SIGMA,
+                *, out=None):
+    """-> (S [N,B-1,K,K] fp32, S0 [N,K] fp32 or None)."""
+    N, B, K, d = in_vec.shape
+    if out is None:
+        S = torch.empty(N, max(B - 1, 0), K, K, dtype=torch.float32, device=in_vec.device)
+        S0 = (torch.empty(N, K, dtype=torch.float32, device=in_vec.device)
+              if anchor_out is not None else None)
+    else:
+        S, S0 = out
+    lilicorr_pair_scores(_dev(in_vec, "in_vec", (torch.float32,)),
+                         _dev(out_vec, "out_vec", (torch.float32,)),
+                         _dev(anchor_out, "anchor_out", (torch.float32,)), N, B, K, d, float(sigma),
+                         _dev(S, "S", (torch.float32,)) if B > 1 else None,
+                         _dev(S0, "S0", (torch.float32,)), _stream())
+    return S, S0
+
+
+def greedy_walk(S: torch.Tensor, S0, logp: torch.Tensor, ids: torch.Tensor,
+                logp_weight: float = 0.0, *, out=None):
+    """-> (draft [N,B] int32, choice [N,B] int32, logq [N,B] fp32)."""
+    N, B, K = ids.shape
+    if out is None:
+        out = (torch.empty(N, B, dtype=torch.int32, device=ids.device),
+               torch.empty(N, B, dtype=torch.int32, device=ids.device),
+               torch.empty(N, B, dtype=torch.float32, device=ids.device))
+    draft, choice, logq = out
+    lilicorr_greedy_walk(_dev(S, "S", (torch.float32,)) if B > 1 else None,
+                         _dev(S0, "S0", (torch.float32,)), _dev(logp, "logp", (torch.float32,)),
+                         _dev(ids, "ids", (torch.int32,)), N, B, K, float(logp_weight),
+                         _dev(draft, "draft", (torch.int32,)), _dev(choice, "choice", (torch.int32,)),
+                         _dev(logq, "logq", (torch.float32,)), _stream())
+    return draft, choice, logq
+
+
+def draft_block(logits: torch.Tensor, K: int, E: torch.Tensor, packed: torch.Tensor,
+                anchor_out=None, sigma: float = SIGMA, logp_weight: float = 0.0):
+    """The whole path on one stream: top-K -> vectors -> pair scores -> greedy walk."""
+    ids, logp = topk(logits, K)
+    in_vec, out_vec = candidate_vectors(ids, E, packed)
+    S, S0 = pair_scores(in_vec, out_vec, anchor_out, sigma)
+    draft, choice, logq = greedy_walk(S, S0, logp, ids, logp_weight)
+    return {"ids": ids, "logp": logp, "in_vec": in_vec, "out_vec": out_vec, "S": S, "S0": S0,
+            "draft": draft, "choice": choice, "logq": logq}

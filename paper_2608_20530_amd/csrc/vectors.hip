@@ -1,0 +1,346 @@
+// Step 2 of the path: candidate in/out vectors. The head's two linear heads emit an out and an in
+// vector per candidate, each normalised to unit norm (Sec. 3.2, implementation appendix); here
+// they are u = E[id] W (W[i][j], row-vector convention) followed by v = u / ||u||.
+//
+// bf16 embeddings: a dense [M x d] x [d x d] contraction per side, run on the bf16 matrix cores
+// (v_mfma_f32_16x16x32_bf16). Every fp32 weight is split exactly into three bf16 terms
+// (hi + mid + lo == w), so each bf16 x bf16 product is exact in fp32 and the fp32 accumulation
+// gives fp32-grade results at three times the MFMA work. A workgroup owns up to 256 candidate
+// rows and all d columns of one side, so the L2 norm of every row is finished in-kernel; the
+// weight slice of each (k-block, term) step is staged once per workgroup in LDS (double buffered)
+// and every wave reuses each B fragment across 4 row blocks and each A fragment (gathered
+// embedding row, loaded straight from HBM) across up to 8 column blocks and the 3 terms.
+//
+// fp32 embeddings: products are no longer exact in bf16, so a plain fp32 FMA kernel is used.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "common.hpp"
+#include "lilicorr.h"
+
+namespace lilicorr {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kRm = 4;        // 16-row blocks per wave
+constexpr int kRn = 8;        // 16-column blocks per wave
+constexpr int kMaxChunks = 8; // 16-byte staging chunks per thread per step
+
+struct VecGeom {
+  int d16, dk, NG, MG;
+};
+
+inline VecGeom vec_geom(int d) {
+  VecGeom g;
+  g.d16 = d / 16;
+  g.dk = (d + 31) / 32;
+  g.NG = (g.d16 + kRn - 1) / kRn;
+  g.MG = 8 / g.NG;
+  if (g.MG < 1) g.MG = 1;
+  return g;
+}
+
+// packed weight layout
+//   [side 2][k-block dk][term 3][column block d16][lane 64][8 bf16]: matrix-core B fragments,
+//     lane l of block (kb, nb) holds W[kb*32 + (l/16)*8 + i][nb*16 + l%16], i = 0..7 (0 beyond d)
+//   followed by [side 2][d][d] fp32 copies (used by the fp32-embedding kernel)
+inline size_t frag_bytes(int d) {
+  VecGeom g = vec_geom(d);
+  return (size_t)2 * g.dk * 3 * g.d16 * 1024;
+}
+
+__device__ __forceinline__ uint16_t split_term(float w, int term) {
+  float hi = __uint_as_float(__float_as_uint(w) & 0xffff0000u);
+  float r1 = w - hi;  // exact: the low 16 significand bits of w
+  float mid = __uint_as_float(__float_as_uint(r1) & 0xffff0000u);
+  float r2 = r1 - mid;  // exact, at most 8 significant bits: a bf16 value
+  float t = term == 0 ? hi : (term == 1 ? mid : r2);
+  return (uint16_t)(__float_as_uint(t) >> 16);
+}
+
+__global__ void pack_weights_kernel(const float* __restrict__ W_in, const float* __restrict__ W_out,
+                                    int d, uint16_t* __restrict__ frags, float* __restrict__ f32copy) {
+  const int d16 = d / 16, dk = (d + 31) / 32;
+  const int64_t nfrag = (int64_t)2 * dk * 3 * d16 * 512;
+  const int64_t ncopy = (int64_t)2 * d * d;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nfrag + ncopy;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (i < nfrag) {
+      int64_t r = i;
+      const int e = (int)(r % 8); r /= 8;
+      const int lane = (int)(r % 64); r /= 64;
+      const int nb = (int)(r % d16); r /= d16;
+      const int term = (int)(r % 3); r /= 3;
+      const int kb = (int)(r % dk); r /= dk;
+      const int side = (int)r;
+      const int k = kb * 32 + (lane / 16) * 8 + e;
+      const int col = nb * 16 + lane % 16;
+      const float* W = side == 0 ? W_in : W_out;
+      const float w = k < d ? W[(int64_t)k * d + col] : 0.f;
+      frags[i] = split_term(w, term);
+    } else {
+      const int64_t j = i - nfrag;
+      const int side = (int)(j / ((int64_t)d * d));
+      const int64_t off = j % ((int64_t)d * d);
+      f32copy[j] = (side == 0 ? W_in : W_out)[off];
+    }
+  }
+}
+
+__global__ __launch_bounds__(512) void cand_vectors_mfma_kernel(
+    const int32_t* __restrict__ ids, const uint16_t* __restrict__ E, const unsigned char* __restrict__ frags,
+    int64_t M, int64_t V, int d, int NG, int MG, float* __restrict__ in_vec, float* __restrict__ out_vec) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int d16 = d / 16, dk = (d + 31) / 32;
+  const int side = blockIdx.y;
+  const int nthreads = NG * MG * kWave;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
+  const int mg = wave / NG, ng = wave % NG;
+  const int nb0 = ng * kRn;
+  const int nbn = (d16 - nb0) < kRn ? (d16 - nb0) : kRn;
+  const int64_t rows_per_wg = (int64_t)MG * kRm * 16;
+  const int64_t row0 = blockIdx.x * rows_per_wg + (int64_t)mg * kRm * 16;
+
+  const size_t slice_bytes = (size_t)d16 * 1024;
+  unsigned char* buf[2] = {smem, smem + slice_bytes};
+  float* ssbuf = reinterpret_cast<float*>(smem + 2 * slice_bytes);  // [MG*64 rows][NG]
+
+  // the embedding row each lane feeds into the A operand of each row block
+  int32_t my_id[kRm];
+#pragma unroll
+  for (int mb = 0; mb < kRm; ++mb) {
+    const int64_t r = row0 + mb * 16 + lane % 16;
+    const int32_t id = r < M ? ids[r] : -1;
+    my_id[mb] = (id >= 0 && id < V) ? id : -1;  // an id outside [0, V) reads nothing
+  }
+
+  f32x4 acc[kRm][kRn];
+#pragma unroll
+  for (int mb = 0; mb < kRm; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < kRn; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const unsigned char* side_frags = frags + (size_t)side * dk * 3 * slice_bytes;
+  const int nchunks = d16 * kWave;  // 16-byte chunks per slice
+  const int nsteps = dk * 3;
+
+  u32x4 stage[kMaxChunks];
+  auto load_slice = [&](int step) {
+    const u32x4* src = reinterpret_cast<const u32x4*>(side_frags + (size_t)step * slice_bytes);
+#pragma unroll
+    for (int c = 0; c < kMaxChunks; ++c) {
+      const int idx = tid + c * nthreads;
+      if (idx < nchunks) stage[c] = src[idx];
+    }
+  };
+  auto store_slice = [&](int step) {
+    u32x4* dst = reinterpret_cast<u32x4*>(buf[step & 1]);
+#pragma unroll
+    for (int c = 0; c < kMaxChunks; ++c) {
+      const int idx = tid + c * nthreads;
+      if (idx < nchunks) dst[idx] = stage[c];
+    }
+  };
+
+  bf16x8 a[kRm];
+  load_slice(0);
+  for (int step = 0; step < nsteps; ++step) {
+    const int kb = step / 3;
+    if (step % 3 == 0) {
+      const int kcol = kb * 32 + (lane / 16) * 8;
+#pragma unroll
+      for (int mb = 0; mb < kRm; ++mb) {
+        if (my_id[mb] >= 0 && kcol < d) {
+          a[mb] = *reinterpret_cast<const bf16x8*>(E + (int64_t)my_id[mb] * d + kcol);
+        } else {
+          a[mb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+        }
+      }
+    }
+    store_slice(step);
+    __syncthreads();
+    if (step + 1 < nsteps) load_slice(step + 1);
+    const u32x4* bs = reinterpret_cast<const u32x4*>(buf[step & 1]);
+#pragma unroll
+    for (int nb = 0; nb < kRn; ++nb) {
+      if (nb < nbn) {
+        const bf16x8 b = __builtin_bit_cast(bf16x8, bs[(nb0 + nb) * kWave + lane]);
+#pragma unroll
+        for (int mb = 0; mb < kRm; ++mb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mb], b, acc[mb][nb], 0, 0, 0);
+      }
+    }
+  }
+
+  // row norms: lane l holds rows (l/16)*4 + i of each row block, column l%16 of each column block
+  const int rows_wg = MG * kRm * 16;
+#pragma unroll
+  for (int mb = 0; mb < kRm; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float ss = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < kRn; ++nb)
+        if (nb < nbn) ss = fmaf(acc[mb][nb][i], acc[mb][nb][i], ss);
+      ss += __shfl_xor(ss, 1, kWave);
+      ss += __shfl_xor(ss, 2, kWave);
+      ss += __shfl_xor(ss, 4, kWave);
+      ss += __shfl_xor(ss, 8, kWave);
+      if ((lane & 15) == 0) ssbuf[(mg * kRm * 16 + mb * 16 + (lane / 16) * 4 + i) * NG + ng] = ss;
+    }
+  }
+  __syncthreads();
+  float* out = side == 0 ? in_vec : out_vec;
+#pragma unroll
+  for (int mb = 0; mb < kRm; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rl = mg * kRm * 16 + mb * 16 + (lane / 16) * 4 + i;
+      float tot = 0.f;
+      for (int g = 0; g < NG; ++g) tot += ssbuf[rl * NG + g];
+      const float inv = tot > 0.f ? 1.0f / sqrtf(tot) : 0.f;
+      const int64_t r = blockIdx.x * (int64_t)rows_wg + rl;
+      if (r < M) {
+#pragma unroll
+        for (int nb = 0; nb < kRn; ++nb)
+          if (nb < nbn) out[r * d + (nb0 + nb) * 16 + (lane & 15)] = acc[mb][nb][i] * inv;
+      }
+    }
+  }
+}
+
+constexpr int kF32Rows = 16;
+constexpr int kF32Threads = 256;
+
+__global__ __launch_bounds__(kF32Threads) void cand_vectors_f32_kernel(
+    const int32_t* __restrict__ ids, const float* __restrict__ E, const float* __restrict__ Wf,
+    int64_t M, int64_t V, int d, float* __restrict__ in_vec, float* __restrict__ out_vec) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  float* e = reinterpret_cast<float*>(smem);       // [16][d]
+  float* part = e + kF32Rows * d;                  // [16][256]
+  float* inv = part + kF32Rows * kF32Threads;      // [16]
+  const int side = blockIdx.y;
+  const int64_t r0 = blockIdx.x * (int64_t)kF32Rows;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kF32Rows * d; i += kF32Threads) {
+    const int r = i / d, c = i % d;
+    const int64_t row = r0 + r;
+    const int32_t id = row < M ? ids[row] : -1;
+    e[i] = (id >= 0 && id < V) ? E[(int64_t)id * d + c] : 0.f;  // outside [0, V): zero row
+  }
+  __syncthreads();
+  const float* W = Wf + (size_t)side * d * d;
+  float u[4][kF32Rows];
+  float ss[kF32Rows];
+#pragma unroll
+  for (int r = 0; r < kF32Rows; ++r) ss[r] = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = tid + q * kF32Threads;
+#pragma unroll
+    for (int r = 0; r < kF32Rows; ++r) u[q][r] = 0.f;
+    if (j < d) {
+      for (int i = 0; i < d; ++i) {
+        const float w = W[(int64_t)i * d + j];
+#pragma unroll
+        for (int r = 0; r < kF32Rows; ++r) u[q][r] = fmaf(e[r * d + i], w, u[q][r]);
+      }
+#pragma unroll
+      for (int r = 0; r < kF32Rows; ++r) ss[r] = fmaf(u[q][r], u[q][r], ss[r]);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kF32Rows; ++r) part[r * kF32Threads + tid] = ss[r];
+  __syncthreads();
+  if (tid < kF32Rows) {
+    float t = 0.f;
+    for (int i = 0; i < kF32Threads; ++i) t += part[tid * kF32Threads + i];
+    inv[tid] = t > 0.f ? 1.0f / sqrtf(t) : 0.f;
+  }
+  __syncthreads();
+  float* out = side == 0 ? in_vec : out_vec;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = tid + q * kF32Threads;
+    if (j < d) {
+#pragma unroll
+      for (int r = 0; r < kF32Rows; ++r) {
+        const int64_t row = r0 + r;
+        if (row < M) out[row * d + j] = u[q][r] * inv[r];
+      }
+    }
+  }
+}
+
+bool vec_d_ok(int d) { return d >= 16 && d <= 1024 && d % 16 == 0; }
+
+}  // namespace
+}  // namespace lilicorr
+
+using namespace lilicorr;
+
+extern "C" size_t lilicorr_packed_weight_bytes(int d) {
+  if (!vec_d_ok(d)) return 0;
+  return frag_bytes(d) + (size_t)2 * d * d * sizeof(float);
+}
+
+extern "C" lilicorr_status lilicorr_pack_weights(const float* W_in, const float* W_out, int d,
+                                                 void* packed, hipStream_t stream) {
+  if (!W_in || !W_out || !packed) return LILICORR_ERR_INVALID_ARG;
+  if (!vec_d_ok(d)) return LILICORR_ERR_UNSUPPORTED;
+  if (!aligned16(W_in) || !aligned16(W_out) || !aligned16(packed)) return LILICORR_ERR_ALIGNMENT;
+  unsigned char* p = static_cast<unsigned char*>(packed);
+  hipLaunchKernelGGL(pack_weights_kernel, dim3(1024), dim3(256), 0, stream, W_in, W_out, d,
+                     reinterpret_cast<uint16_t*>(p), reinterpret_cast<float*>(p + frag_bytes(d)));
+  return launch_status();
+}
+
+extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const void* E,
+                                                      lilicorr_dtype e_dtype, int64_t V, int d,
+                                                      const void* packed_w, int64_t N, int64_t B,
+                                                      int K, float* in_vec, float* out_vec,
+                                                      hipStream_t stream) {
+  if (!ids || !E || !packed_w || !in_vec || !out_vec) return LILICORR_ERR_INVALID_ARG;
+  if (e_dtype != LILICORR_F32 && e_dtype != LILICORR_BF16) return LILICORR_ERR_INVALID_ARG;
+  if (N < 1 || B < 1 || K < 1 || V < 1) return LILICORR_ERR_INVALID_ARG;
+  if (!vec_d_ok(d) || K > 64 || V >= ((int64_t)1 << 31)) return LILICORR_ERR_UNSUPPORTED;
+  if (N > ((int64_t)1 << 40) / B) return LILICORR_ERR_UNSUPPORTED;
+  const int64_t M = N * B * K;
+  if (M > ((int64_t)1 << 40)) return LILICORR_ERR_UNSUPPORTED;
+  if (!aligned16(ids) || !aligned16(E) || !aligned16(packed_w) || !aligned16(in_vec) ||
+      !aligned16(out_vec))
+    return LILICORR_ERR_ALIGNMENT;
+  const unsigned char* p = static_cast<const unsigned char*>(packed_w);
+  if (e_dtype == LILICORR_BF16) {
+    VecGeom g = vec_geom(d);
+    const int64_t rows_wg = (int64_t)g.MG * kRm * 16;
+    const int64_t nblk = (M + rows_wg - 1) / rows_wg;
+    if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
+    const size_t lds = 2 * (size_t)g.d16 * 1024 + (size_t)rows_wg * g.NG * sizeof(float);
+    static const hipError_t attr_mfma = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(cand_vectors_mfma_kernel),
+        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)attr_mfma;
+    hipLaunchKernelGGL(cand_vectors_mfma_kernel, dim3((unsigned)nblk, 2), dim3(g.NG * g.MG * kWave),
+                       lds, stream, ids, static_cast<const uint16_t*>(E), p, M, V, d, g.NG, g.MG,
+                       in_vec, out_vec);
+  } else {
+    const int64_t nblk = (M + kF32Rows - 1) / kF32Rows;
+    if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
+    const size_t lds = ((size_t)kF32Rows * d + kF32Rows * kF32Threads + kF32Rows) * sizeof(float);
+    static const hipError_t attr_f32 = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(cand_vectors_f32_kernel),
+        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)attr_f32;
+    hipLaunchKernelGGL(cand_vectors_f32_kernel, dim3((unsigned)nblk, 2), dim3(kF32Threads), lds,
+                       stream, ids, static_cast<const float*>(E),
+                       reinterpret_cast<const float*>(p + frag_bytes(d)), M, V, d, in_vec, out_vec);
+  }
+  return launch_status();
+}

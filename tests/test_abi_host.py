@@ -1,0 +1,122 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every symbol that
+include/lilicorr.h declares, and rejects bad arguments before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lilicorr.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(lilicorr_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2608_20530_amd as L
+
+    L.load_library()
+    return L
+
+
+def test_header_declares_the_path(L):
+    names = _declared()
+    for n in ["lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_pack_weights",
+              "lilicorr_packed_weight_bytes", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
+              "lilicorr_greedy_walk", "lilicorr_status_string"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(L):
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in _declared():
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(L):
+    assert L.lilicorr_status_string(0) == "ok"
+    for code in (-1, -2, -3, -4, -5):
+        assert L.lilicorr_status_string(code) not in ("ok", "unknown status")
+    assert L.lilicorr_status_string(-99) == "unknown status"
+
+
+def test_size_queries(L):
+    assert L.lilicorr_packed_weight_bytes(256) == 2 * 3 * 256 * 256 * 2 + 2 * 256 * 256 * 4
+    assert L.lilicorr_packed_weight_bytes(48) == 2 * 3 * 64 * 48 * 2 + 2 * 48 * 48 * 4
+    assert L.lilicorr_packed_weight_bytes(8) == 0
+    assert L.lilicorr_packed_weight_bytes(2048) == 0
+    # headline shapes run one workgroup per row: no workspace
+    assert L.lilicorr_topk_workspace_bytes(64, 16, 151936, 16) == 0
+    assert L.lilicorr_topk_workspace_bytes(256, 16, 262144, 32) == 0
+    # a single request is split over several workgroups per row
+    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) > 0
+    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 65) == 0
+
+
+A = 4096  # a fake, 16-byte aligned "device" address: never dereferenced on these paths
+
+
+def test_topk_argument_errors(L):
+    lib = L.load_library()
+    ok = (A, 1, 2, 3, 1000, 8, A, A, None, 0, None)
+    def call(i, v):
+        args = list(ok)
+        args[i] = v
+        return lib.lilicorr_topk(*args)
+    assert call(0, None) == -1          # logits
+    assert call(6, None) == -1          # ids
+    assert call(7, None) == -1          # logp
+    assert call(1, 7) == -1             # dtype
+    assert call(2, 0) == -1             # N
+    assert call(3, 0) == -1             # B
+    assert call(4, 0) == -1             # V
+    assert call(5, 0) == -1             # K
+    assert call(5, 65) == -2            # K > 64
+    assert call(5, 1001) == -2          # K > V
+    assert call(0, A + 2) == -3         # alignment
+    # N*B*V that would need workspace, none given
+    args = list(ok)
+    args[2], args[3], args[4] = 1, 1, 151936
+    assert lib.lilicorr_topk(*args) == -4
+
+
+def test_other_argument_errors(L):
+    lib = L.load_library()
+    assert lib.lilicorr_pack_weights(None, A, 64, A, None) == -1
+    assert lib.lilicorr_pack_weights(A, A, 40, A, None) == -2
+    assert lib.lilicorr_pack_weights(A, A + 4, 64, A, None) == -3
+    cv = [A, A, 1, 1000, 64, A, 2, 3, 4, A, A, None]
+    assert lib.lilicorr_candidate_vectors(*cv[:2], 5, *cv[3:]) == -1
+    bad = list(cv); bad[4] = 2048
+    assert lib.lilicorr_candidate_vectors(*bad) == -2
+    bad = list(cv); bad[9] = A + 8
+    assert lib.lilicorr_candidate_vectors(*bad) == -3
+    ps = [A, A, None, 2, 3, 4, 64, 8.0, A, None, None]
+    bad = list(ps); bad[8] = None
+    assert lib.lilicorr_pair_scores(*bad) == -1   # S required when B > 1
+    bad = list(ps); bad[2] = A
+    assert lib.lilicorr_pair_scores(*bad) == -1   # S0 required with an anchor
+    bad = list(ps); bad[7] = float("nan")
+    assert lib.lilicorr_pair_scores(*bad) == -1
+    bad = list(ps); bad[6] = 24
+    assert lib.lilicorr_pair_scores(*bad) == -2
+    gw = [A, None, A, A, 2, 3, 4, 0.0, A, None, None, None]
+    bad = list(gw); bad[0] = None
+    assert lib.lilicorr_greedy_walk(*bad) == -1   # S required when B > 1
+    bad = list(gw); bad[6] = 65
+    assert lib.lilicorr_greedy_walk(*bad) == -2
+    bad = list(gw); bad[8] = A + 4
+    assert lib.lilicorr_greedy_walk(*bad) == -3
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    import paper_2608_20530_amd as L
+
+    monkeypatch.setattr(L, "_lib", None)
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(L.LilicorrError):
+        L.load_library()

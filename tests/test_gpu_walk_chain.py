@@ -1,0 +1,126 @@
+"""GPU parity of step 4 (lilicorr_greedy_walk) and of the whole chain against the oracle.
+
+Walk: on identical S / S0 / logp / ids the draft and choice are bit-exact and logq is within
+1e-5 * max(1, |logq|). Chain: the GPU runs topk -> candidate_vectors -> pair_scores ->
+greedy_walk on one stream and the oracle runs its own chain on the same seeded inputs; drafts
+must be bit-exact at every config (configs 3-4 compared on sampled requests, each request's
+oracle chain computed on its own). A mismatch reports the oracle's top-2 score gap at the
+decision where the two walks part.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+import yaml
+
+import oracle
+import workloads
+from parity import assert_close, assert_equal, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _walk(lib, S, S0, logp, ids, lam=0.0):
+    c = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    out = lib.greedy_walk(c(S), c(S0), c(logp), c(ids), lam)
+    torch.cuda.synchronize()
+    return [to_np(o) for o in out]
+
+
+@pytest.mark.parametrize("N,B,K,anchor,lam,coarse", [
+    (1, 1, 1, False, 0.0, False), (3, 2, 2, True, 0.0, True), (16, 16, 16, False, 0.0, True),
+    (7, 16, 32, True, 0.0, False), (5, 9, 64, True, 0.0, True), (4, 30, 64, False, 0.0, False),
+    (8, 16, 8, True, 1.0, False), (2, 6, 5, False, -0.5, True),
+])
+def test_walk_random(lib, N, B, K, anchor, lam, coarse):
+    print(f"walk N={N} B={B} K={K} anchor={anchor} lam={lam}", flush=True)
+    rng = np.random.default_rng(N * 100 + K)
+    if coarse:
+        S = (rng.integers(-4, 5, size=(N, B - 1, K, K)) * 2.0).astype(np.float32)
+    else:
+        S = (rng.standard_normal((N, B - 1, K, K)) * 3).astype(np.float32)
+    S0 = rng.standard_normal((N, K)).astype(np.float32) if anchor else None
+    logp = -np.sort(rng.random((N, B, K)) * 5, axis=-1).astype(np.float32)
+    ids = rng.integers(0, 150000, size=(N, B, K)).astype(np.int32)
+    gd, gc, gq = _walk(lib, S, S0, logp, ids, lam)
+    rd, rc, rq = oracle.greedy_walk(S, S0, logp, ids, lam)
+    assert_equal(gc, rc, "choice")
+    assert_equal(gd, rd, "draft")
+    assert_close(gq, rq, "logq")
+
+
+def test_walk_hand_cases(lib, golden_dir):
+    cases = yaml.safe_load(open(os.path.join(golden_dir, "walk_hand_cases.yaml")))["cases"]
+    for c in cases:
+        S = np.array(c["S"], np.float32)[None]
+        B = S.shape[1] + 1
+        K = S.shape[-1]
+        S0 = None if c["S0"] is None else np.array(c["S0"], np.float32)[None]
+        ids = np.array(c.get("ids", np.arange(B * K).reshape(B, K)), np.int32)[None]
+        gd, gc, gq = _walk(lib, S, S0, np.zeros((1, B, K), np.float32), ids)
+        assert gc[0].tolist() == c["choice"], c["name"]
+        if "draft" in c:
+            assert gd[0].tolist() == c["draft"], c["name"]
+        if "logq" in c:
+            assert_close(gq[0], np.array(c["logq"]), c["name"])
+        if "logq0" in c:
+            assert_close(gq[0, :1], np.array([c["logq0"]]), c["name"])
+
+
+def _oracle_chain(logits_np, E, W_in, W_out, K, anchor=None):
+    ids, logp = oracle.topk(logits_np, K)
+    iv, ov = oracle.candidate_vectors(ids, E, W_in, W_out)
+    S, S0 = oracle.pair_scores(iv, ov, anchor, 8.0)
+    draft, choice, logq = oracle.greedy_walk(S, S0, logp, ids)
+    return dict(ids=ids, logp=logp, S=S, S0=S0, draft=draft, choice=choice, logq=logq)
+
+
+def _explain(gpu, ref, n):
+    """Where the walks part: the oracle's top-2 gap of the node scores at that decision."""
+    t = int(np.argmax(gpu["choice"][n] != ref["choice"][n]))
+    if t == 0:
+        z = ref["S0"][n] if ref["S0"] is not None else np.zeros(ref["ids"].shape[-1])
+    else:
+        z = ref["S"][n, t - 1, ref["choice"][n, t - 1]]
+    top = np.sort(z.astype(np.float64))[::-1]
+    return f"request {n} slot {t}: oracle top-2 gap {top[0] - top[1]:.3e}"
+
+
+@pytest.mark.parametrize("cfg_index", [0, 1, 2, 3, 4])
+def test_chain_drafts_bit_exact(lib, cfg_inputs, cfg_index):
+    cfg, inp = cfg_inputs(cfg_index)
+    print(f"chain config {cfg_index} {cfg.name}", flush=True)
+    logits = inp["logits"].cuda()
+    E = inp["E"].cuda()
+    packed = lib.pack_weights(inp["W_in"].cuda(), inp["W_out"].cuda())
+    out = lib.draft_block(logits, cfg.K, E, packed)
+    torch.cuda.synchronize()
+    g = {k: (to_np(v) if v is not None else None) for k, v in out.items()}
+    del logits
+    reqs = list(range(cfg.N)) if cfg.N <= 16 else sorted(
+        set([0, 1, 2, cfg.N - 1] + np.random.default_rng(cfg_index).choice(cfg.N, 4, replace=False).tolist()))
+    E_np, W_in, W_out = to_np(inp["E"]), to_np(inp["W_in"]), to_np(inp["W_out"])
+    lg = to_np(inp["logits"])
+    for n in reqs:
+        r = _oracle_chain(lg[n:n + 1], E_np, W_in, W_out, cfg.K)
+        sub = {k: (v[n:n + 1] if v is not None else None) for k, v in g.items()}
+        assert_equal(sub["ids"], r["ids"], f"cfg{cfg_index} req {n} ids")
+        assert_close(sub["logp"], r["logp"], f"cfg{cfg_index} req {n} logp")
+        assert_close(sub["S"], r["S"], f"cfg{cfg_index} req {n} S")
+        if not np.array_equal(sub["choice"], r["choice"]):
+            raise AssertionError(f"cfg{cfg_index} draft differs: " + _explain(sub, r, 0))
+        assert_equal(sub["draft"], r["draft"], f"cfg{cfg_index} req {n} draft")
+        assert_close(sub["logq"], r["logq"], f"cfg{cfg_index} req {n} logq")
+
+
+def test_chain_with_anchor(lib, cfg_inputs):
+    cfg, inp = cfg_inputs(1)
+    anchor = workloads.make_anchor(cfg)
+    packed = lib.pack_weights(inp["W_in"].cuda(), inp["W_out"].cuda())
+    out = lib.draft_block(inp["logits"].cuda(), cfg.K, inp["E"].cuda(), packed, anchor.cuda())
+    torch.cuda.synchronize()
+    r = _oracle_chain(to_np(inp["logits"]), to_np(inp["E"]), to_np(inp["W_in"]),
+                      to_np(inp["W_out"]), cfg.K, to_np(anchor))
+    assert_close(to_np(out["S0"]), r["S0"], "S0")
+    assert_equal(to_np(out["draft"]), r["draft"], "draft with anchor")
