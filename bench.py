@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the LiLiCorr draft-correlation hot path on one MI355X.
+
+One step = the whole path over one batch of synthetic input, on one stream:
+    lilicorr_topk -> lilicorr_candidate_vectors -> lilicorr_pair_scores -> lilicorr_greedy_walk
+for the headline workload (N = 64 requests, B = 16 slots, K = 16 candidates, V = 151936,
+d = 256, bf16 logits). The metric is scored draft blocks per second (N blocks per step). Logits
+rotate over four resident copies (1.2 GB, above the 256 MB Infinity Cache) so every step streams
+its logits from HBM; the embedding table and packed weights stay resident, as served weights do.
+
+Printed: one JSON line with the step throughput, a roofline entry for the dominant kernel (the
+logits pass, timed with HIP events around each of its launches on the launch stream), the
+logits-pass bandwidth at the stress workload (N = 256, K = 32, V = 262144), and the CPU oracle
+timed on a bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "scored draft blocks/sec at N=64,B=16,K=16,V=151936; logits-pass HBM GB/s"
+PEAK_HBM_GBS = 8000.0
+ROTATE = 4
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "topk_lse_headline64_traffic.json")
+TOPK_SRC = os.path.join(ROOT, "paper_2608_20530_amd", "csrc", "topk.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-stress", action="store_true", help="skip the stress logits-pass line")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
+    return ap.parse_args()
+
+
+def topk_kernel_hash() -> str:
+    return hashlib.sha256(open(TOPK_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_per_launch():
+    """HBM bytes per logits-pass launch from the committed counter summary, or None when the
+    kernel source changed since the counters were taken."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("topk_source_sha256_16") != topk_kernel_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def time_logits_pass(L, torch, cfg, logits_list, iters, warmup):
+    """Average duration (s) of the logits-pass kernel over `iters` cold launches."""
+    K = cfg.K
+    N, B, V = logits_list[0].shape
+    ids = torch.empty(N, B, K, dtype=torch.int32, device="cuda")
+    logp = torch.empty(N, B, K, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(L.lilicorr_topk_workspace_bytes(N, B, V, K), 16), dtype=torch.uint8,
+                     device="cuda")
+    for i in range(warmup):
+        L.topk(logits_list[i % len(logits_list)], K, out=(ids, logp), workspace=ws)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+    torch.cuda.synchronize()
+    for i in range(iters):
+        ev[i][0].record()
+        L.topk(logits_list[i % len(logits_list)], K, out=(ids, logp), workspace=ws)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    return statistics.mean(a.elapsed_time(b) for a, b in ev) / 1e3
+
+
+def cpu_baseline(cfg, inp, seconds):
+    """The oracle chain, single-threaded, on whole requests of the workload until `seconds`."""
+    import numpy as np
+
+    import oracle
+
+    lg = inp["logits"].view(__import__("torch").int16).numpy().view(np.uint16)
+    E = inp["E"].view(__import__("torch").int16).numpy().view(np.uint16)
+    W_in, W_out = inp["W_in"].numpy(), inp["W_out"].numpy()
+    oracle.topk(lg[:1, :1, :64], 4)  # load/compile outside the timing
+    done = 0
+    t0 = time.perf_counter()
+    while done < cfg.N:
+        x = lg[done:done + 1]
+        ids, logp = oracle.topk(x, cfg.K)
+        iv, ov = oracle.candidate_vectors(ids, E, W_in, W_out)
+        S, S0 = oracle.pair_scores(iv, ov, None, 8.0)
+        oracle.greedy_walk(S, S0, logp, ids)
+        done += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "blocks/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of {cfg.N} requests of the headline workload (whole chain per "
+                      f"request, fp64, single thread), {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this path has no multi-GPU mode (asked for "
+              f"--gpus {args.gpus}); the sharding design is in the design notes", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2608_20530_amd as L
+    import workloads
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    L.load_library()
+
+    cfg = workloads.config(3)
+    t_gen = time.perf_counter()
+    inp = workloads.make_inputs(cfg)
+    t_gen = time.perf_counter() - t_gen
+    N, B, K, V, d = cfg.N, cfg.B, cfg.K, cfg.V, cfg.d
+    logits0 = inp["logits"].cuda()
+    logits_list = [logits0] + [logits0.clone() for _ in range(ROTATE - 1)]
+    E = inp["E"].cuda()
+    packed = L.pack_weights(inp["W_in"].cuda(), inp["W_out"].cuda())
+
+    dev = "cuda"
+    ids = torch.empty(N, B, K, dtype=torch.int32, device=dev)
+    logp = torch.empty(N, B, K, dtype=torch.float32, device=dev)
+    ws = torch.empty(max(L.lilicorr_topk_workspace_bytes(N, B, V, K), 16), dtype=torch.uint8, device=dev)
+    in_vec = torch.empty(N, B, K, d, dtype=torch.float32, device=dev)
+    out_vec = torch.empty_like(in_vec)
+    S = torch.empty(N, B - 1, K, K, dtype=torch.float32, device=dev)
+    draft = torch.empty(N, B, dtype=torch.int32, device=dev)
+    choice = torch.empty_like(draft)
+    logq = torch.empty(N, B, dtype=torch.float32, device=dev)
+
+    def step(i, ev=None):
+        if ev is not None:
+            ev[0].record()
+        L.topk(logits_list[i % ROTATE], K, out=(ids, logp), workspace=ws)
+        if ev is not None:
+            ev[1].record()
+        L.candidate_vectors(ids, E, packed, out=(in_vec, out_vec))
+        L.pair_scores(in_vec, out_vec, None, L.SIGMA, out=(S, None))
+        L.greedy_walk(S, None, logp, ids, 0.0, out=(draft, choice, logq))
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    print(f"[bench] timed {args.steps} steps in {elapsed:.4f} s", file=sys.stderr, flush=True)
+
+    ms_per_step = elapsed / args.steps * 1e3
+    value = N * args.steps / elapsed
+    topk_s = statistics.mean(a.elapsed_time(b) for a, b in evs) / 1e3
+    logits_bytes = N * B * V * 2
+    algo_bytes = logits_bytes + N * B * K * 8
+    achieved = algo_bytes / topk_s / 1e9
+    traffic = traffic_per_launch()
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "blocks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "headline: N=64 requests, B=16 slots, K=16, V=151936, d=256, "
+                               "bf16 logits (3 entropy tiers, 1% exact ties), bf16 embeddings, "
+                               "fp32 weights; no anchor; sigma=8",
+                   "N": N, "B": B, "K": K, "V": V, "d": d, "logits_dtype": "bf16",
+                   "logits_rotation": ROTATE},
+        "roofline": {"bound": "hbm", "kernel": "topk_lse_kernel", "achieved": achieved,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": traffic, "avg_launch_us": topk_s * 1e6,
+                     "algorithmic_bytes_per_launch": algo_bytes},
+    }
+
+    if not args.no_stress:
+        c4 = workloads.config(4)
+        t = time.perf_counter()
+        lg4 = workloads.make_logits(c4).cuda()
+        print(f"[bench] stress logits generated in {time.perf_counter() - t:.1f} s", file=sys.stderr,
+              flush=True)
+        t3 = time_logits_pass(L, torch, cfg, logits_list, iters=50, warmup=5)
+        del logits_list
+        torch.cuda.empty_cache()
+        t4 = time_logits_pass(L, torch, c4, [lg4], iters=20, warmup=3)
+        b4 = c4.N * c4.B * c4.V * 2 + c4.N * c4.B * c4.K * 8
+        out["logits_pass"] = {
+            "headline": {"GB_s": algo_bytes / t3 / 1e9, "us": t3 * 1e6,
+                         "frac_of_8TBs": algo_bytes / t3 / 1e9 / PEAK_HBM_GBS},
+            "stress": {"GB_s": b4 / t4 / 1e9, "us": t4 * 1e6,
+                       "frac_of_8TBs": b4 / t4 / 1e9 / PEAK_HBM_GBS,
+                       "workload": "N=256, B=16, K=32, V=262144, bf16 logits"},
+        }
+        del lg4
+
+    if args.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(cfg, inp, args.cpu_seconds)
+
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

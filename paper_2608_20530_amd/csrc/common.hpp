@@ -73,6 +73,74 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Wave-wide reductions on DPP (row shifts within 16-lane rows, then row broadcasts); the result
+// lands in lane 63 and is read back as a wave-uniform value. Lanes a DPP step cannot source
+// receive the identity.
+template <int CTRL, int ROW_MASK, int BANK_MASK>
+__device__ __forceinline__ float dpp_f32(float identity, float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(identity), __float_as_int(x),
+                                                    CTRL, ROW_MASK, BANK_MASK, false));
+}
+
+template <typename Op>
+__device__ __forceinline__ float wave_reduce_dpp(float v, float identity, Op op) {
+  // after the row shifts by 1, 2, 4, 8 lane 15 of each 16-lane row holds that row's total
+  v = op(v, dpp_f32<0x111, 0xf, 0xf>(identity, v));  // row_shr:1
+  v = op(v, dpp_f32<0x112, 0xf, 0xf>(identity, v));  // row_shr:2
+  v = op(v, dpp_f32<0x114, 0xf, 0xf>(identity, v));  // row_shr:4
+  v = op(v, dpp_f32<0x118, 0xf, 0xf>(identity, v));  // row_shr:8
+  v = op(v, dpp_f32<0x142, 0xa, 0xf>(identity, v));  // row_bcast:15 into rows 1 and 3
+  v = op(v, dpp_f32<0x143, 0xc, 0xf>(identity, v));  // row_bcast:31 into rows 2 and 3
+  return readlanef(v, 63);
+}
+
+__device__ __forceinline__ float wave_max_dpp(float v) {
+  return wave_reduce_dpp(v, -__builtin_inff(), [](float a, float b) { return fmaxf(a, b); });
+}
+
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  return wave_reduce_dpp(v, 0.f, [](float a, float b) { return a + b; });
+}
+
+// ---- staging global memory into LDS ------------------------------------------------------------
+// Every thread issues up to BATCH independent loads before its first LDS store, so a staging pass
+// costs one memory round trip per batch instead of one per element.
+typedef unsigned int stage_u32x4 __attribute__((ext_vector_type(4)));
+
+template <int BATCH, typename T>
+__device__ __forceinline__ void stage_to_lds(T* __restrict__ dst, const T* __restrict__ src,
+                                             int64_t n, int tid, int nthreads) {
+  for (int64_t base = tid; base < n; base += (int64_t)BATCH * nthreads) {
+    T v[BATCH];
+#pragma unroll
+    for (int b = 0; b < BATCH; ++b) {
+      const int64_t i = base + (int64_t)b * nthreads;
+      if (i < n) v[b] = src[i];
+    }
+#pragma unroll
+    for (int b = 0; b < BATCH; ++b) {
+      const int64_t i = base + (int64_t)b * nthreads;
+      if (i < n) dst[i] = v[b];
+    }
+  }
+}
+
+// As stage_to_lds for 4-byte words, moving 16-byte chunks when both addresses allow it.
+__device__ __forceinline__ void stage_words(void* dst, const void* src, int64_t nwords, int tid,
+                                            int nthreads) {
+  if (((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15u) == 0) {
+    const int64_t n16 = nwords / 4;
+    stage_to_lds<8>(static_cast<stage_u32x4*>(dst), static_cast<const stage_u32x4*>(src), n16, tid,
+                    nthreads);
+    const int64_t done = n16 * 4;
+    if (tid < nwords - done)
+      static_cast<uint32_t*>(dst)[done + tid] = static_cast<const uint32_t*>(src)[done + tid];
+  } else {
+    stage_to_lds<8>(static_cast<uint32_t*>(dst), static_cast<const uint32_t*>(src), nwords, tid,
+                    nthreads);
+  }
+}
+
 // ---- candidate keys ---------------------------------------------------------------------------
 // A candidate (value x, token id) is ranked by x descending, then id ascending. The 64-bit key
 //   (order(x) << 32) | (0xFFFFFFFF - id)
@@ -111,6 +179,21 @@ __device__ __forceinline__ uint64_t merge_desc64(uint64_t a, uint64_t b) {
     c = lower ? (c > o ? c : o) : (c < o ? c : o);
   }
   return c;
+}
+
+// Full descending bitonic sort of one 64-bit key per lane.
+__device__ __forceinline__ uint64_t sort_desc64_u64(uint64_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j >= 1; j >>= 1) {
+      const uint64_t o = shfl_xor64(v, j);
+      const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
+      v = keep_max ? (v > o ? v : o) : (v < o ? v : o);
+    }
+  }
+  return v;
 }
 
 // Full descending bitonic sort of one float per lane.

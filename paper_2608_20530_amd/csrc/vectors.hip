@@ -26,21 +26,19 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRm = 4;        // 16-row blocks per wave
-constexpr int kRn = 8;        // 16-column blocks per wave
-constexpr int kMaxChunks = 8; // 16-byte staging chunks per thread per step
+constexpr int kNbPerWave = 4;  // 16-column blocks owned by each wave
 
 struct VecGeom {
-  int d16, dk, NG, MG;
+  int d16, dk, waves, rm;
 };
 
+// waves = one per 4 column blocks; 128 rows per workgroup up to d = 512, 64 rows above
 inline VecGeom vec_geom(int d) {
   VecGeom g;
   g.d16 = d / 16;
   g.dk = (d + 31) / 32;
-  g.NG = (g.d16 + kRn - 1) / kRn;
-  g.MG = 8 / g.NG;
-  if (g.MG < 1) g.MG = 1;
+  g.waves = (g.d16 + kNbPerWave - 1) / kNbPerWave;
+  g.rm = g.waves <= 8 ? 8 : 4;
   return g;
 }
 
@@ -91,124 +89,140 @@ __global__ void pack_weights_kernel(const float* __restrict__ W_in, const float*
   }
 }
 
-__global__ __launch_bounds__(512) void cand_vectors_mfma_kernel(
-    const int32_t* __restrict__ ids, const uint16_t* __restrict__ E, const unsigned char* __restrict__ frags,
-    int64_t M, int64_t V, int d, int NG, int MG, float* __restrict__ in_vec, float* __restrict__ out_vec) {
+// One workgroup: RM*16 candidate rows x all d columns of one side. The gathered embedding rows
+// (the A operand) are staged once in LDS; wave w owns column blocks [4w, 4w+4) and streams their
+// B fragments (three bf16 terms per block) straight from the L2-resident packed weights, one
+// k-block ahead of the MFMAs that use them. Each B fragment feeds RM MFMAs and each A fragment 12.
+template <int RM, int MAXT>
+__global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
+    const int32_t* __restrict__ ids, const uint16_t* __restrict__ E,
+    const unsigned char* __restrict__ frags, int64_t M, int64_t V, int d,
+    float* __restrict__ in_vec, float* __restrict__ out_vec) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  constexpr int ROWS = RM * 16;
   const int d16 = d / 16, dk = (d + 31) / 32;
+  const int dpad = dk * 32;
+  const int astride = dpad + 8;  // bf16 elements per LDS row (16-byte multiple, spreads banks)
   const int side = blockIdx.y;
-  const int nthreads = NG * MG * kWave;
+  const int nthreads = blockDim.x;
+  const int nwaves = nthreads / kWave;
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid / kWave;
-  const int mg = wave / NG, ng = wave % NG;
-  const int nb0 = ng * kRn;
-  const int nbn = (d16 - nb0) < kRn ? (d16 - nb0) : kRn;
-  const int64_t rows_per_wg = (int64_t)MG * kRm * 16;
-  const int64_t row0 = blockIdx.x * rows_per_wg + (int64_t)mg * kRm * 16;
+  const int nb0 = wave * kNbPerWave;
+  const int nbn = (d16 - nb0) < kNbPerWave ? (d16 - nb0) : kNbPerWave;
+  const int64_t row0 = blockIdx.x * (int64_t)ROWS;
 
-  const size_t slice_bytes = (size_t)d16 * 1024;
-  unsigned char* buf[2] = {smem, smem + slice_bytes};
-  float* ssbuf = reinterpret_cast<float*>(smem + 2 * slice_bytes);  // [MG*64 rows][NG]
+  uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [ROWS][astride]
+  float* ssbuf = reinterpret_cast<float*>(smem + (size_t)ROWS * astride * 2);  // [nwaves][ROWS]
+  int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + nwaves * ROWS);             // [ROWS]
 
-  // the embedding row each lane feeds into the A operand of each row block
-  int32_t my_id[kRm];
-#pragma unroll
-  for (int mb = 0; mb < kRm; ++mb) {
-    const int64_t r = row0 + mb * 16 + lane % 16;
-    const int32_t id = r < M ? ids[r] : -1;
-    my_id[mb] = (id >= 0 && id < V) ? id : -1;  // an id outside [0, V) reads nothing
+  // gather the embedding rows (zero rows past M or for ids outside [0, V); zero k-padding):
+  // the ids first, then eight independent 16-byte row loads in flight per thread
+  for (int r = tid; r < ROWS; r += nthreads) {
+    const int64_t row = row0 + r;
+    const int32_t id = row < M ? ids[row] : -1;
+    rid[r] = (id >= 0 && id < V) ? id : -1;
   }
-
-  f32x4 acc[kRm][kRn];
+  __syncthreads();
+  const int cpr = dpad / 8;  // 16-byte chunks per LDS row
+  for (int i0 = tid; i0 < ROWS * cpr; i0 += 8 * nthreads) {
+    u32x4 v[8];
 #pragma unroll
-  for (int mb = 0; mb < kRm; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < kRn; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const unsigned char* side_frags = frags + (size_t)side * dk * 3 * slice_bytes;
-  const int nchunks = d16 * kWave;  // 16-byte chunks per slice
-  const int nsteps = dk * 3;
-
-  u32x4 stage[kMaxChunks];
-  auto load_slice = [&](int step) {
-    const u32x4* src = reinterpret_cast<const u32x4*>(side_frags + (size_t)step * slice_bytes);
-#pragma unroll
-    for (int c = 0; c < kMaxChunks; ++c) {
-      const int idx = tid + c * nthreads;
-      if (idx < nchunks) stage[c] = src[idx];
-    }
-  };
-  auto store_slice = [&](int step) {
-    u32x4* dst = reinterpret_cast<u32x4*>(buf[step & 1]);
-#pragma unroll
-    for (int c = 0; c < kMaxChunks; ++c) {
-      const int idx = tid + c * nthreads;
-      if (idx < nchunks) dst[idx] = stage[c];
-    }
-  };
-
-  bf16x8 a[kRm];
-  load_slice(0);
-  for (int step = 0; step < nsteps; ++step) {
-    const int kb = step / 3;
-    if (step % 3 == 0) {
-      const int kcol = kb * 32 + (lane / 16) * 8;
-#pragma unroll
-      for (int mb = 0; mb < kRm; ++mb) {
-        if (my_id[mb] >= 0 && kcol < d) {
-          a[mb] = *reinterpret_cast<const bf16x8*>(E + (int64_t)my_id[mb] * d + kcol);
-        } else {
-          a[mb] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-        }
+    for (int b = 0; b < 8; ++b) {
+      const int i = i0 + b * nthreads;
+      v[b] = u32x4{0u, 0u, 0u, 0u};
+      if (i < ROWS * cpr) {
+        const int r = i / cpr, c = i - r * cpr;
+        const int32_t id = rid[r];
+        if (id >= 0 && c * 8 < d) v[b] = *reinterpret_cast<const u32x4*>(E + (int64_t)id * d + c * 8);
       }
     }
-    store_slice(step);
-    __syncthreads();
-    if (step + 1 < nsteps) load_slice(step + 1);
-    const u32x4* bs = reinterpret_cast<const u32x4*>(buf[step & 1]);
 #pragma unroll
-    for (int nb = 0; nb < kRn; ++nb) {
-      if (nb < nbn) {
-        const bf16x8 b = __builtin_bit_cast(bf16x8, bs[(nb0 + nb) * kWave + lane]);
-#pragma unroll
-        for (int mb = 0; mb < kRm; ++mb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mb], b, acc[mb][nb], 0, 0, 0);
+    for (int b = 0; b < 8; ++b) {
+      const int i = i0 + b * nthreads;
+      if (i < ROWS * cpr) {
+        const int r = i / cpr, c = i - r * cpr;
+        *reinterpret_cast<u32x4*>(A + r * astride + c * 8) = v[b];
       }
+    }
+  }
+  __syncthreads();
+
+  f32x4 acc[RM][kNbPerWave];
+#pragma unroll
+  for (int mb = 0; mb < RM; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const size_t slice = (size_t)d16 * 1024;  // one (k-block, term) slice of fragments
+  const unsigned char* fr = frags + (size_t)side * dk * 3 * slice;
+  u32x4 b[kNbPerWave][3], bn[kNbPerWave][3];
+  auto load_b = [&](u32x4 (&dst)[kNbPerWave][3], int kb) {
+#pragma unroll
+    for (int nb = 0; nb < kNbPerWave; ++nb)
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+        if (nb < nbn)
+          dst[nb][t] = *reinterpret_cast<const u32x4*>(fr + ((size_t)kb * 3 + t) * slice +
+                                                       (size_t)(nb0 + nb) * 1024 + lane * 16);
+  };
+  if (nbn > 0) load_b(b, 0);
+  for (int kb = 0; kb < dk; ++kb) {
+    if (nbn > 0 && kb + 1 < dk) load_b(bn, kb + 1);
+    if (nbn > 0) {
+      const int kcol = kb * 32 + (lane >> 4) * 8;
+#pragma unroll
+      for (int mb = 0; mb < RM; ++mb) {
+        const bf16x8 a = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(A + (mb * 16 + (lane & 15)) * astride + kcol));
+#pragma unroll
+        for (int nb = 0; nb < kNbPerWave; ++nb)
+          if (nb < nbn)
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  a, __builtin_bit_cast(bf16x8, b[nb][t]), acc[mb][nb], 0, 0, 0);
+      }
+    }
+    if (kb + 1 < dk) {
+#pragma unroll
+      for (int nb = 0; nb < kNbPerWave; ++nb)
+#pragma unroll
+        for (int t = 0; t < 3; ++t) b[nb][t] = bn[nb][t];
     }
   }
 
   // row norms: lane l holds rows (l/16)*4 + i of each row block, column l%16 of each column block
-  const int rows_wg = MG * kRm * 16;
 #pragma unroll
-  for (int mb = 0; mb < kRm; ++mb) {
+  for (int mb = 0; mb < RM; ++mb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float ss = 0.f;
 #pragma unroll
-      for (int nb = 0; nb < kRn; ++nb)
+      for (int nb = 0; nb < kNbPerWave; ++nb)
         if (nb < nbn) ss = fmaf(acc[mb][nb][i], acc[mb][nb][i], ss);
       ss += __shfl_xor(ss, 1, kWave);
       ss += __shfl_xor(ss, 2, kWave);
       ss += __shfl_xor(ss, 4, kWave);
       ss += __shfl_xor(ss, 8, kWave);
-      if ((lane & 15) == 0) ssbuf[(mg * kRm * 16 + mb * 16 + (lane / 16) * 4 + i) * NG + ng] = ss;
+      if ((lane & 15) == 0) ssbuf[wave * ROWS + mb * 16 + (lane >> 4) * 4 + i] = ss;
     }
   }
   __syncthreads();
   float* out = side == 0 ? in_vec : out_vec;
 #pragma unroll
-  for (int mb = 0; mb < kRm; ++mb) {
+  for (int mb = 0; mb < RM; ++mb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int rl = mg * kRm * 16 + mb * 16 + (lane / 16) * 4 + i;
+      const int rl = mb * 16 + (lane >> 4) * 4 + i;
       float tot = 0.f;
-      for (int g = 0; g < NG; ++g) tot += ssbuf[rl * NG + g];
+      for (int g = 0; g < nwaves; ++g) tot += ssbuf[g * ROWS + rl];
       const float inv = tot > 0.f ? 1.0f / sqrtf(tot) : 0.f;
-      const int64_t r = blockIdx.x * (int64_t)rows_wg + rl;
+      const int64_t r = row0 + rl;
       if (r < M) {
 #pragma unroll
-        for (int nb = 0; nb < kRn; ++nb)
+        for (int nb = 0; nb < kNbPerWave; ++nb)
           if (nb < nbn) out[r * d + (nb0 + nb) * 16 + (lane & 15)] = acc[mb][nb][i] * inv;
       }
     }
@@ -318,18 +332,29 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
     return LILICORR_ERR_ALIGNMENT;
   const unsigned char* p = static_cast<const unsigned char*>(packed_w);
   if (e_dtype == LILICORR_BF16) {
-    VecGeom g = vec_geom(d);
-    const int64_t rows_wg = (int64_t)g.MG * kRm * 16;
+    const VecGeom g = vec_geom(d);
+    const int64_t rows_wg = (int64_t)g.rm * 16;
     const int64_t nblk = (M + rows_wg - 1) / rows_wg;
     if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
-    const size_t lds = 2 * (size_t)g.d16 * 1024 + (size_t)rows_wg * g.NG * sizeof(float);
-    static const hipError_t attr_mfma = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(cand_vectors_mfma_kernel),
-        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    (void)attr_mfma;
-    hipLaunchKernelGGL(cand_vectors_mfma_kernel, dim3((unsigned)nblk, 2), dim3(g.NG * g.MG * kWave),
-                       lds, stream, ids, static_cast<const uint16_t*>(E), p, M, V, d, g.NG, g.MG,
-                       in_vec, out_vec);
+    const size_t lds = (size_t)rows_wg * (g.dk * 32 + 8) * 2 + (size_t)g.waves * rows_wg * sizeof(float) +
+                       (size_t)rows_wg * sizeof(int32_t);
+    const dim3 grid((unsigned)nblk, 2), block(g.waves * kWave);
+    const uint16_t* e16 = static_cast<const uint16_t*>(E);
+    if (g.rm == 8) {
+      static const hipError_t attr8 = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(cand_vectors_mfma_kernel<8, 512>),
+          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      (void)attr8;
+      hipLaunchKernelGGL((cand_vectors_mfma_kernel<8, 512>), grid, block, lds, stream, ids, e16, p,
+                         M, V, d, in_vec, out_vec);
+    } else {
+      static const hipError_t attr4 = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(cand_vectors_mfma_kernel<4, 1024>),
+          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      (void)attr4;
+      hipLaunchKernelGGL((cand_vectors_mfma_kernel<4, 1024>), grid, block, lds, stream, ids, e16, p,
+                         M, V, d, in_vec, out_vec);
+    }
   } else {
     const int64_t nblk = (M + kF32Rows - 1) / kF32Rows;
     if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
