@@ -5,11 +5,12 @@
 // bf16 embeddings: a dense [M x d] x [d x d] contraction per side, run on the bf16 matrix cores
 // (v_mfma_f32_16x16x32_bf16). Every fp32 weight is split exactly into three bf16 terms
 // (hi + mid + lo == w), so each bf16 x bf16 product is exact in fp32 and the fp32 accumulation
-// gives fp32-grade results at three times the MFMA work. A workgroup owns up to 256 candidate
-// rows and all d columns of one side, so the L2 norm of every row is finished in-kernel; the
-// weight slice of each (k-block, term) step is staged once per workgroup in LDS (double buffered)
-// and every wave reuses each B fragment across 4 row blocks and each A fragment (gathered
-// embedding row, loaded straight from HBM) across up to 8 column blocks and the 3 terms.
+// gives fp32-grade results at three times the MFMA work. A workgroup owns a tile of candidate rows
+// and all d columns of one side, so the L2 norm of every row is finished in-kernel. The gathered
+// embedding rows (the A operand) are staged once in LDS; each wave owns four 16-column blocks and
+// streams their B fragments (three terms each) from the L2-resident packed weights through two
+// register buffers, loading k-block kb+1 while the MFMAs of kb run. The packed layout is padded to
+// whole wave column groups and an even number of k-blocks, so the MFMA loop has no branches.
 //
 // fp32 embeddings: products are no longer exact in bf16, so a plain fp32 FMA kernel is used.
 #include <hip/hip_runtime.h>
@@ -29,26 +30,36 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kNbPerWave = 4;  // 16-column blocks owned by each wave
 
 struct VecGeom {
-  int d16, dk, waves, rm;
+  int d16;    // 16-column blocks of the output
+  int nbp;    // d16 rounded up to whole waves (kNbPerWave blocks each)
+  int dk;     // 32-deep k-blocks of the contraction
+  int dkp;    // dk rounded up to even (the MFMA loop handles two k-blocks per trip)
+  int waves;  // waves per workgroup: one per kNbPerWave column blocks
+  int rm;     // 16-row blocks per workgroup
 };
 
-// waves = one per 4 column blocks; 128 rows per workgroup up to d = 512, 64 rows above
-inline VecGeom vec_geom(int d) {
+// rm: up to d = 512, 128-row tiles once there are enough of them to give every compute unit
+// several (a workgroup's phases, gather -> MFMA -> store, then overlap with other workgroups'),
+// else 64-row tiles, which put two workgroups on each compute unit; 32-row tiles above d = 512
+inline VecGeom vec_geom(int d, int64_t M = 0) {
   VecGeom g;
   g.d16 = d / 16;
+  g.nbp = (g.d16 + kNbPerWave - 1) / kNbPerWave * kNbPerWave;
   g.dk = (d + 31) / 32;
-  g.waves = (g.d16 + kNbPerWave - 1) / kNbPerWave;
-  g.rm = g.waves <= 8 ? 8 : 4;
+  g.dkp = (g.dk + 1) / 2 * 2;
+  g.waves = g.nbp / kNbPerWave;
+  g.rm = d > 512 ? 2 : ((M + 127) / 128 * 2 >= 2048 ? 8 : 4);
   return g;
 }
 
 // packed weight layout
-//   [side 2][k-block dk][term 3][column block d16][lane 64][8 bf16]: matrix-core B fragments,
-//     lane l of block (kb, nb) holds W[kb*32 + (l/16)*8 + i][nb*16 + l%16], i = 0..7 (0 beyond d)
+//   [side 2][k-block dkp][term 3][column block nbp][lane 64][8 bf16]: matrix-core B fragments,
+//     lane l of block (kb, nb) holds W[kb*32 + (l/16)*8 + i][nb*16 + l%16], i = 0..7
+//     (0 for rows or columns at or beyond d)
 //   followed by [side 2][d][d] fp32 copies (used by the fp32-embedding kernel)
 inline size_t frag_bytes(int d) {
   VecGeom g = vec_geom(d);
-  return (size_t)2 * g.dk * 3 * g.d16 * 1024;
+  return (size_t)2 * g.dkp * 3 * g.nbp * 1024;
 }
 
 __device__ __forceinline__ uint16_t split_term(float w, int term) {
@@ -61,9 +72,9 @@ __device__ __forceinline__ uint16_t split_term(float w, int term) {
 }
 
 __global__ void pack_weights_kernel(const float* __restrict__ W_in, const float* __restrict__ W_out,
-                                    int d, uint16_t* __restrict__ frags, float* __restrict__ f32copy) {
-  const int d16 = d / 16, dk = (d + 31) / 32;
-  const int64_t nfrag = (int64_t)2 * dk * 3 * d16 * 512;
+                                    int d, int nbp, int dkp, uint16_t* __restrict__ frags,
+                                    float* __restrict__ f32copy) {
+  const int64_t nfrag = (int64_t)2 * dkp * 3 * nbp * 512;
   const int64_t ncopy = (int64_t)2 * d * d;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nfrag + ncopy;
        i += (int64_t)gridDim.x * blockDim.x) {
@@ -71,14 +82,14 @@ __global__ void pack_weights_kernel(const float* __restrict__ W_in, const float*
       int64_t r = i;
       const int e = (int)(r % 8); r /= 8;
       const int lane = (int)(r % 64); r /= 64;
-      const int nb = (int)(r % d16); r /= d16;
+      const int nb = (int)(r % nbp); r /= nbp;
       const int term = (int)(r % 3); r /= 3;
-      const int kb = (int)(r % dk); r /= dk;
+      const int kb = (int)(r % dkp); r /= dkp;
       const int side = (int)r;
       const int k = kb * 32 + (lane / 16) * 8 + e;
       const int col = nb * 16 + lane % 16;
       const float* W = side == 0 ? W_in : W_out;
-      const float w = k < d ? W[(int64_t)k * d + col] : 0.f;
+      const float w = (k < d && col < d) ? W[(int64_t)k * d + col] : 0.f;
       frags[i] = split_term(w, term);
     } else {
       const int64_t j = i - nfrag;
@@ -89,19 +100,51 @@ __global__ void pack_weights_kernel(const float* __restrict__ W_in, const float*
   }
 }
 
+typedef u32x4 BFrag[kNbPerWave][3];
+
+// B fragments of k-block kb for the wave's four column blocks, three terms each
+__device__ __forceinline__ void load_bfrag(BFrag& dst, const unsigned char* wf, size_t slice,
+                                           int kb) {
+  const unsigned char* p = wf + (size_t)kb * 3 * slice;
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int nb = 0; nb < kNbPerWave; ++nb)
+      dst[nb][t] = *reinterpret_cast<const u32x4*>(p + t * slice + nb * 1024);
+}
+
+// acc[mb][nb] += A[rows of block mb][k-block kb] x B[k-block kb][column block nb], all three
+// terms; the term loop is outermost so consecutive MFMAs never feed each other
+template <int RM>
+__device__ __forceinline__ void mfma_kblock(f32x4 (&acc)[RM][kNbPerWave], const BFrag& b,
+                                            const uint16_t* A, int astride, int kb, int lane) {
+  bf16x8 a[RM];
+  const int kcol = kb * 32 + (lane >> 4) * 8;
+#pragma unroll
+  for (int mb = 0; mb < RM; ++mb)
+    a[mb] = __builtin_bit_cast(
+        bf16x8, *reinterpret_cast<const u32x4*>(A + (mb * 16 + (lane & 15)) * astride + kcol));
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int mb = 0; mb < RM; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kNbPerWave; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            a[mb], __builtin_bit_cast(bf16x8, b[nb][t]), acc[mb][nb], 0, 0, 0);
+}
+
 // One workgroup: RM*16 candidate rows x all d columns of one side. The gathered embedding rows
-// (the A operand) are staged once in LDS; wave w owns column blocks [4w, 4w+4) and streams their
-// B fragments (three bf16 terms per block) straight from the L2-resident packed weights, one
-// k-block ahead of the MFMAs that use them. Each B fragment feeds RM MFMAs and each A fragment 12.
+// (the A operand) are staged once in LDS; wave w owns column blocks [4w, 4w+4). Each B fragment
+// feeds RM MFMAs and each A fragment 12.
 template <int RM, int MAXT>
 __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
     const int32_t* __restrict__ ids, const uint16_t* __restrict__ E,
-    const unsigned char* __restrict__ frags, int64_t M, int64_t V, int d,
+    const unsigned char* __restrict__ frags, int64_t M, int64_t V, int d, int nbp, int dkp,
     float* __restrict__ in_vec, float* __restrict__ out_vec) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   constexpr int ROWS = RM * 16;
-  const int d16 = d / 16, dk = (d + 31) / 32;
-  const int dpad = dk * 32;
+  const int dpad = dkp * 32;
   const int astride = dpad + 8;  // bf16 elements per LDS row (16-byte multiple, spreads banks)
   const int side = blockIdx.y;
   const int nthreads = blockDim.x;
@@ -109,13 +152,18 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid / kWave;
-  const int nb0 = wave * kNbPerWave;
-  const int nbn = (d16 - nb0) < kNbPerWave ? (d16 - nb0) : kNbPerWave;
   const int64_t row0 = blockIdx.x * (int64_t)ROWS;
 
   uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [ROWS][astride]
   float* ssbuf = reinterpret_cast<float*>(smem + (size_t)ROWS * astride * 2);  // [nwaves][ROWS]
   int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + nwaves * ROWS);             // [ROWS]
+
+  // this wave's fragments: column blocks [4 wave, 4 wave + 4) of one (k-block, term) slice
+  const size_t slice = (size_t)nbp * 1024;
+  const unsigned char* wf =
+      frags + (size_t)side * dkp * 3 * slice + (size_t)wave * kNbPerWave * 1024 + lane * 16;
+  BFrag b0, b1;
+  load_bfrag(b0, wf, slice, 0);  // in flight during the gather
 
   // gather the embedding rows (zero rows past M or for ids outside [0, V); zero k-padding):
   // the ids first, then eight independent 16-byte row loads in flight per thread
@@ -129,21 +177,21 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   for (int i0 = tid; i0 < ROWS * cpr; i0 += 8 * nthreads) {
     u32x4 v[8];
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const int i = i0 + b * nthreads;
-      v[b] = u32x4{0u, 0u, 0u, 0u};
+    for (int q = 0; q < 8; ++q) {
+      const int i = i0 + q * nthreads;
+      v[q] = u32x4{0u, 0u, 0u, 0u};
       if (i < ROWS * cpr) {
         const int r = i / cpr, c = i - r * cpr;
         const int32_t id = rid[r];
-        if (id >= 0 && c * 8 < d) v[b] = *reinterpret_cast<const u32x4*>(E + (int64_t)id * d + c * 8);
+        if (id >= 0 && c * 8 < d) v[q] = *reinterpret_cast<const u32x4*>(E + (int64_t)id * d + c * 8);
       }
     }
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const int i = i0 + b * nthreads;
+    for (int q = 0; q < 8; ++q) {
+      const int i = i0 + q * nthreads;
       if (i < ROWS * cpr) {
         const int r = i / cpr, c = i - r * cpr;
-        *reinterpret_cast<u32x4*>(A + r * astride + c * 8) = v[b];
+        *reinterpret_cast<u32x4*>(A + r * astride + c * 8) = v[q];
       }
     }
   }
@@ -155,53 +203,25 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
 #pragma unroll
     for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const size_t slice = (size_t)d16 * 1024;  // one (k-block, term) slice of fragments
-  const unsigned char* fr = frags + (size_t)side * dk * 3 * slice;
-  u32x4 b[kNbPerWave][3], bn[kNbPerWave][3];
-  auto load_b = [&](u32x4 (&dst)[kNbPerWave][3], int kb) {
-#pragma unroll
-    for (int nb = 0; nb < kNbPerWave; ++nb)
-#pragma unroll
-      for (int t = 0; t < 3; ++t)
-        if (nb < nbn)
-          dst[nb][t] = *reinterpret_cast<const u32x4*>(fr + ((size_t)kb * 3 + t) * slice +
-                                                       (size_t)(nb0 + nb) * 1024 + lane * 16);
-  };
-  if (nbn > 0) load_b(b, 0);
-  for (int kb = 0; kb < dk; ++kb) {
-    if (nbn > 0 && kb + 1 < dk) load_b(bn, kb + 1);
-    if (nbn > 0) {
-      const int kcol = kb * 32 + (lane >> 4) * 8;
-#pragma unroll
-      for (int mb = 0; mb < RM; ++mb) {
-        const bf16x8 a = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(A + (mb * 16 + (lane & 15)) * astride + kcol));
-#pragma unroll
-        for (int nb = 0; nb < kNbPerWave; ++nb)
-          if (nb < nbn)
-#pragma unroll
-            for (int t = 0; t < 3; ++t)
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  a, __builtin_bit_cast(bf16x8, b[nb][t]), acc[mb][nb], 0, 0, 0);
-      }
-    }
-    if (kb + 1 < dk) {
-#pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb)
-#pragma unroll
-        for (int t = 0; t < 3; ++t) b[nb][t] = bn[nb][t];
-    }
+  // two k-blocks per trip through two register buffers: the loads of the next k-block are in
+  // flight while the MFMAs of the current one run (the last trip reloads the final k-block
+  // instead of reading past the packed weights)
+  for (int kb = 0; kb < dkp; kb += 2) {
+    load_bfrag(b1, wf, slice, kb + 1);
+    mfma_kblock<RM>(acc, b0, A, astride, kb, lane);
+    load_bfrag(b0, wf, slice, kb + 2 < dkp ? kb + 2 : dkp - 1);
+    mfma_kblock<RM>(acc, b1, A, astride, kb + 1, lane);
   }
 
   // row norms: lane l holds rows (l/16)*4 + i of each row block, column l%16 of each column block
+  // (padding columns hold zeros)
 #pragma unroll
   for (int mb = 0; mb < RM; ++mb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float ss = 0.f;
 #pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb)
-        if (nb < nbn) ss = fmaf(acc[mb][nb][i], acc[mb][nb][i], ss);
+      for (int nb = 0; nb < kNbPerWave; ++nb) ss = fmaf(acc[mb][nb][i], acc[mb][nb][i], ss);
       ss += __shfl_xor(ss, 1, kWave);
       ss += __shfl_xor(ss, 2, kWave);
       ss += __shfl_xor(ss, 4, kWave);
@@ -211,6 +231,7 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   }
   __syncthreads();
   float* out = side == 0 ? in_vec : out_vec;
+  const int col0 = wave * kNbPerWave * 16 + (lane & 15);
 #pragma unroll
   for (int mb = 0; mb < RM; ++mb) {
 #pragma unroll
@@ -223,7 +244,7 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
       if (r < M) {
 #pragma unroll
         for (int nb = 0; nb < kNbPerWave; ++nb)
-          if (nb < nbn) out[r * d + (nb0 + nb) * 16 + (lane & 15)] = acc[mb][nb][i] * inv;
+          if (col0 + nb * 16 < d) out[r * d + col0 + nb * 16] = acc[mb][nb][i] * inv;
       }
     }
   }
@@ -310,8 +331,10 @@ extern "C" lilicorr_status lilicorr_pack_weights(const float* W_in, const float*
   if (!vec_d_ok(d)) return LILICORR_ERR_UNSUPPORTED;
   if (!aligned16(W_in) || !aligned16(W_out) || !aligned16(packed)) return LILICORR_ERR_ALIGNMENT;
   unsigned char* p = static_cast<unsigned char*>(packed);
-  hipLaunchKernelGGL(pack_weights_kernel, dim3(1024), dim3(256), 0, stream, W_in, W_out, d,
-                     reinterpret_cast<uint16_t*>(p), reinterpret_cast<float*>(p + frag_bytes(d)));
+  const VecGeom g = vec_geom(d);
+  hipLaunchKernelGGL(pack_weights_kernel, dim3(1024), dim3(256), 0, stream, W_in, W_out, d, g.nbp,
+                     g.dkp, reinterpret_cast<uint16_t*>(p),
+                     reinterpret_cast<float*>(p + frag_bytes(d)));
   return launch_status();
 }
 
@@ -332,12 +355,12 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
     return LILICORR_ERR_ALIGNMENT;
   const unsigned char* p = static_cast<const unsigned char*>(packed_w);
   if (e_dtype == LILICORR_BF16) {
-    const VecGeom g = vec_geom(d);
+    const VecGeom g = vec_geom(d, M);
     const int64_t rows_wg = (int64_t)g.rm * 16;
     const int64_t nblk = (M + rows_wg - 1) / rows_wg;
     if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
-    const size_t lds = (size_t)rows_wg * (g.dk * 32 + 8) * 2 + (size_t)g.waves * rows_wg * sizeof(float) +
-                       (size_t)rows_wg * sizeof(int32_t);
+    const size_t lds = (size_t)rows_wg * (g.dkp * 32 + 8) * 2 +
+                       (size_t)g.waves * rows_wg * sizeof(float) + (size_t)rows_wg * sizeof(int32_t);
     const dim3 grid((unsigned)nblk, 2), block(g.waves * kWave);
     const uint16_t* e16 = static_cast<const uint16_t*>(E);
     if (g.rm == 8) {
@@ -346,14 +369,21 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
       (void)attr8;
       hipLaunchKernelGGL((cand_vectors_mfma_kernel<8, 512>), grid, block, lds, stream, ids, e16, p,
-                         M, V, d, in_vec, out_vec);
-    } else {
+                         M, V, d, g.nbp, g.dkp, in_vec, out_vec);
+    } else if (g.rm == 4) {
       static const hipError_t attr4 = hipFuncSetAttribute(
-          reinterpret_cast<const void*>(cand_vectors_mfma_kernel<4, 1024>),
+          reinterpret_cast<const void*>(cand_vectors_mfma_kernel<4, 512>),
           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
       (void)attr4;
-      hipLaunchKernelGGL((cand_vectors_mfma_kernel<4, 1024>), grid, block, lds, stream, ids, e16, p,
-                         M, V, d, in_vec, out_vec);
+      hipLaunchKernelGGL((cand_vectors_mfma_kernel<4, 512>), grid, block, lds, stream, ids, e16, p,
+                         M, V, d, g.nbp, g.dkp, in_vec, out_vec);
+    } else {
+      static const hipError_t attr2 = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(cand_vectors_mfma_kernel<2, 1024>),
+          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      (void)attr2;
+      hipLaunchKernelGGL((cand_vectors_mfma_kernel<2, 1024>), grid, block, lds, stream, ids, e16, p,
+                         M, V, d, g.nbp, g.dkp, in_vec, out_vec);
     }
   } else {
     const int64_t nblk = (M + kF32Rows - 1) / kF32Rows;

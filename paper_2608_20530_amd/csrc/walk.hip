@@ -1,11 +1,13 @@
 // Step 4 of the path: greedy left-to-right walk over the candidate lattice (Sec. 3.5) with the
 // local log-likelihood of Eq. (localar).
 //
-// One workgroup per request. Everything a request's walk reads (its score matrices S[n], the
-// candidate ids, the anchor scores and, when they are weighted in, the drafter log-probabilities)
-// is first staged into LDS with coalesced loads, so the B dependent argmax steps touch only LDS
-// and registers; lane k of wave 0 owns candidate k, and the max / sum reductions run on DPP.
-// The outputs of all slots are written at the end with one coalesced store each.
+// The walk's choice at slot t depends only on its choice at t-1, through one row of S. So every
+// row the walk could visit, (slot t, previous choice p), is resolved first, all in parallel: its
+// argmax (lowest index on ties) and its local log-likelihood -log sum_k exp(z_k - max z). Each row
+// is handled by a group of 16, 32 or 64 lanes (one lane per candidate) with DPP butterflies, and
+// the results go to an LDS table. One lane then follows the table, one LDS read per slot, and the
+// whole workgroup writes the slots' outputs. One workgroup per request; slots are processed in
+// segments whose table fits in LDS.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -17,102 +19,106 @@ namespace lilicorr {
 namespace {
 
 constexpr int kWalkThreads = 256;
-constexpr size_t kWalkLdsMax = 96 * 1024;
+constexpr int kSegRows = 2048;  // table rows per segment (slots per segment: kSegRows / K)
+constexpr int kRowBatch = 16;   // rows per group whose loads are issued together
 
-struct WalkPlan {
-  size_t s_bytes, ids_bytes, lp_bytes, out_bytes;
-  int stage_s, stage_ids;
-  size_t lds() const {
-    return (stage_s ? s_bytes : 0) + (stage_ids ? ids_bytes + lp_bytes : 0) + out_bytes;
-  }
-};
-
-inline WalkPlan walk_plan(int64_t B, int K, bool use_logp) {
-  WalkPlan p;
-  p.s_bytes = (size_t)(B - 1) * K * K * sizeof(float);
-  p.ids_bytes = (size_t)B * K * sizeof(int32_t);
-  p.lp_bytes = use_logp ? (size_t)B * K * sizeof(float) : 0;
-  p.out_bytes = B <= 1024 ? (size_t)B * 2 * sizeof(int32_t) + (size_t)B * sizeof(float) : 0;
-  p.stage_ids = p.ids_bytes + p.lp_bytes + p.out_bytes <= kWalkLdsMax / 2;
-  p.stage_s = B > 1 && p.s_bytes + (p.stage_ids ? p.ids_bytes + p.lp_bytes : 0) + p.out_bytes <= kWalkLdsMax;
-  return p;
+// all-reduce over aligned groups of G lanes; every lane of a group receives the group's result
+template <typename Op>
+__device__ __forceinline__ float dpp_allreduce16(float v, Op op) {
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false)));   // quad_perm 1,0,3,2
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xf, 0xf, false)));   // quad_perm 2,3,0,1
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xf, 0xf, false)));  // row_half_mirror
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xf, 0xf, false)));  // row_mirror
+  return v;
 }
 
+template <int G, typename Op>
+__device__ __forceinline__ float group_allreduce(float v, Op op) {
+  v = dpp_allreduce16(v, op);
+  if (G >= 32) v = op(v, __shfl_xor(v, 16, kWave));
+  if (G >= 64) v = op(v, __shfl_xor(v, 32, kWave));
+  return v;
+}
+
+template <int G>
 __global__ __launch_bounds__(kWalkThreads) void greedy_walk_kernel(
     const float* __restrict__ S, const float* __restrict__ S0, const float* __restrict__ logp,
-    const int32_t* __restrict__ ids, int64_t B, int K, float lambda, WalkPlan plan,
+    const int32_t* __restrict__ ids, int64_t B, int K, float lambda,
     int32_t* __restrict__ draft, int32_t* __restrict__ choice, float* __restrict__ logq) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  // row table: low 32 bits the argmax, high 32 bits the fp32 local log-likelihood
+  __shared__ uint64_t table[kSegRows + 1];
+  __shared__ int32_t seg_choice[kSegRows];
+  __shared__ float seg_logq[kSegRows];
+
   const int64_t n = blockIdx.x;
-  const int64_t per_req = (B - 1) * (int64_t)K * K;
-  const float* Sn = S ? S + n * per_req : nullptr;
-  const int32_t* idn = ids + n * B * K;
-  const float* lpn = logp + n * B * K;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int j = tid % G;                 // candidate index within the row
+  const int group = tid / G;
+  constexpr int kGroups = kWalkThreads / G;
+  const int gshift = (lane / G) * G;     // first ballot bit of this lane's group
+  const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
+  const bool live = j < K;
   const bool use_lp = lambda != 0.f;
+  const float* Sn = S ? S + n * (B - 1) * (int64_t)K * K : nullptr;
+  const float* lpn = logp + n * B * K;
+  const int64_t T = kSegRows / K > 0 ? kSegRows / K : 1;  // slots per segment
 
-  unsigned char* p = smem;
-  float* s_lds = reinterpret_cast<float*>(p);
-  if (plan.stage_s) p += plan.s_bytes;
-  int32_t* id_lds = reinterpret_cast<int32_t*>(p);
-  float* lp_lds = reinterpret_cast<float*>(p + plan.ids_bytes);
-  if (plan.stage_ids) p += plan.ids_bytes + plan.lp_bytes;
-  int32_t* o_draft = reinterpret_cast<int32_t*>(p);
-  int32_t* o_choice = o_draft + B;
-  float* o_logq = reinterpret_cast<float*>(o_choice + B);
-  const bool out_lds = plan.out_bytes > 0;
-
-  if (plan.stage_s) stage_words(s_lds, Sn, per_req, threadIdx.x, kWalkThreads);
-  if (plan.stage_ids) {
-    stage_words(id_lds, idn, B * K, threadIdx.x, kWalkThreads);
-    if (use_lp) stage_words(lp_lds, lpn, B * K, threadIdx.x, kWalkThreads);
-  }
-  __syncthreads();
-
-  if (threadIdx.x < kWave) {
-    const int lane = lane_id();
-    const bool live = lane < K;
-    int prev = 0;
-    for (int64_t t = 0; t < B; ++t) {
-      float pair = 0.f;
-      if (live) {
-        if (t == 0) {
-          pair = S0 ? S0[n * K + lane] : 0.f;
-        } else {
-          const int64_t off = ((t - 1) * K + prev) * (int64_t)K + lane;
-          pair = plan.stage_s ? s_lds[off] : Sn[off];
+  int c = 0;  // the walk's current choice (used by thread 0)
+  for (int64_t t0 = 0; t0 < B; t0 += T) {
+    const int64_t t1 = t0 + T < B ? t0 + T : B;
+    // global rows: 0 is slot 0; 1 + (t-1) K + p is slot t >= 1 after choice p
+    const int64_t rb = t0 == 0 ? 0 : 1 + (t0 - 1) * K;
+    const int64_t re = 1 + (t1 - 1) * K;
+    // the trip count is the same for every thread, so whole waves stay converged for the
+    // butterflies and ballots
+    for (int64_t base = rb; base < re; base += (int64_t)kRowBatch * kGroups) {
+      float z[kRowBatch];
+#pragma unroll
+      for (int u = 0; u < kRowBatch; ++u) {
+        const int64_t row = base + group + (int64_t)u * kGroups;
+        float v = -__builtin_inff();
+        if (live && row < re) {
+          if (row == 0) {
+            v = S0 ? S0[n * K + j] : 0.f;
+            if (use_lp) v = fmaf(lambda, lpn[j], v);
+          } else {
+            v = Sn[(row - 1) * K + j];
+            if (use_lp) v = fmaf(lambda, lpn[(1 + (row - 1) / K) * K + j], v);
+          }
         }
+        z[u] = v;
       }
-      float z = pair;
-      if (use_lp && live)
-        z = fmaf(lambda, plan.stage_ids ? lp_lds[t * K + lane] : lpn[t * K + lane], pair);
-      if (!live) z = -__builtin_inff();
-      const float m = wave_max_dpp(z);
-      int c = __ffsll((long long)__ballot(live && z == m)) - 1;
-      if (c < 0) c = 0;  // only reachable with NaN scores; keeps every access in bounds
-      const float s = wave_sum_dpp(live ? expf(z - m) : 0.f);
-      const int32_t tok = plan.stage_ids ? id_lds[t * K + c] : idn[t * K + c];
-      if (lane == 0) {
-        const float lq = -logf(s);
-        if (out_lds) {
-          o_draft[t] = tok;
-          o_choice[t] = c;
-          o_logq[t] = lq;
-        } else {
-          draft[n * B + t] = tok;
-          if (choice) choice[n * B + t] = c;
-          if (logq) logq[n * B + t] = lq;
-        }
+#pragma unroll
+      for (int u = 0; u < kRowBatch; ++u) {
+        const int64_t row = base + group + (int64_t)u * kGroups;
+        const float m = group_allreduce<G>(z[u], [](float a, float b) { return fmaxf(a, b); });
+        const uint64_t hits = (__ballot(live && z[u] == m) >> gshift) & gmask;
+        const int arg = hits ? __ffsll((long long)hits) - 1 : 0;  // no hit only with NaN scores
+        const float s = group_allreduce<G>(live ? expf(z[u] - m) : 0.f,
+                                           [](float a, float b) { return a + b; });
+        if (j == 0 && row < re)
+          table[row - rb] = (uint64_t)(uint32_t)arg | ((uint64_t)__float_as_uint(-logf(s)) << 32);
       }
-      prev = c;
     }
-  }
-  if (out_lds) {
     __syncthreads();
-    for (int64_t t = threadIdx.x; t < B; t += kWalkThreads) {
-      draft[n * B + t] = o_draft[t];
-      if (choice) choice[n * B + t] = o_choice[t];
-      if (logq) logq[n * B + t] = o_logq[t];
+    if (tid == 0) {
+      for (int64_t t = t0; t < t1; ++t) {
+        const int64_t row = t == 0 ? 0 : 1 + (t - 1) * K + c;
+        const uint64_t e = table[row - rb];
+        c = (int)(uint32_t)e;
+        seg_choice[t - t0] = c;
+        seg_logq[t - t0] = __uint_as_float((uint32_t)(e >> 32));
+      }
     }
+    __syncthreads();
+    for (int64_t t = t0 + tid; t < t1; t += kWalkThreads) {
+      const int ct = seg_choice[t - t0];
+      draft[n * B + t] = ids[(n * B + t) * K + ct];
+      if (choice) choice[n * B + t] = ct;
+      if (logq) logq[n * B + t] = seg_logq[t - t0];
+    }
+    __syncthreads();
   }
 }
 
@@ -134,12 +140,15 @@ extern "C" lilicorr_status lilicorr_greedy_walk(const float* S, const float* S0,
   if ((S && !aligned16(S)) || (S0 && !aligned16(S0)) || !aligned16(logp) || !aligned16(ids) ||
       !aligned16(draft) || (choice && !aligned16(choice)) || (logq && !aligned16(logq)))
     return LILICORR_ERR_ALIGNMENT;
-  const WalkPlan plan = walk_plan(B, K, logp_weight != 0.f);
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(greedy_walk_kernel),
-      hipFuncAttributeMaxDynamicSharedMemorySize, (int)kWalkLdsMax);
-  (void)attr;
-  hipLaunchKernelGGL(greedy_walk_kernel, dim3((unsigned)N), dim3(kWalkThreads), plan.lds(), stream,
-                     S, S0, logp, ids, B, K, logp_weight, plan, draft, choice, logq);
+  const dim3 grid((unsigned)N), block(kWalkThreads);
+  if (K <= 16)
+    hipLaunchKernelGGL(greedy_walk_kernel<16>, grid, block, 0, stream, S, S0, logp, ids, B, K,
+                       logp_weight, draft, choice, logq);
+  else if (K <= 32)
+    hipLaunchKernelGGL(greedy_walk_kernel<32>, grid, block, 0, stream, S, S0, logp, ids, B, K,
+                       logp_weight, draft, choice, logq);
+  else
+    hipLaunchKernelGGL(greedy_walk_kernel<64>, grid, block, 0, stream, S, S0, logp, ids, B, K,
+                       logp_weight, draft, choice, logq);
   return launch_status();
 }

@@ -46,7 +46,10 @@ def test_status_strings(L):
 
 def test_size_queries(L):
     assert L.lilicorr_packed_weight_bytes(256) == 2 * 3 * 256 * 256 * 2 + 2 * 256 * 256 * 4
-    assert L.lilicorr_packed_weight_bytes(48) == 2 * 3 * 64 * 48 * 2 + 2 * 48 * 48 * 4
+    # fragments padded to an even number of 32-deep k-blocks and whole groups of four
+    # 16-column blocks: d = 48 -> 64 x 64 per term
+    assert L.lilicorr_packed_weight_bytes(48) == 2 * 3 * 64 * 64 * 2 + 2 * 48 * 48 * 4
+    assert L.lilicorr_packed_weight_bytes(80) == 2 * 3 * 128 * 128 * 2 + 2 * 80 * 80 * 4
     assert L.lilicorr_packed_weight_bytes(8) == 0
     assert L.lilicorr_packed_weight_bytes(2048) == 0
     # headline shapes run one workgroup per row: no workspace

@@ -44,6 +44,11 @@ def test_vectors_configs(lib, cfg_inputs, cfg_index):
 @pytest.mark.parametrize("d,K,N,B,e_dtype", [
     (16, 1, 1, 1, "bf16"), (48, 5, 2, 3, "bf16"), (64, 7, 3, 5, "bf16"), (1024, 3, 2, 4, "bf16"),
     (512, 32, 1, 9, "bf16"), (96, 4, 2, 2, "f32"), (1024, 2, 1, 3, "f32"), (16, 3, 1, 2, "f32"),
+    # padded column groups and k-blocks: d = 80 (5 -> 8 column blocks, 3 -> 4 k-blocks),
+    # d = 272 (17 -> 20, 9 -> 10), d = 1008 (63 -> 64, 32)
+    (80, 9, 3, 7, "bf16"), (272, 16, 2, 5, "bf16"), (1008, 4, 2, 3, "bf16"),
+    # enough rows for the 128-row tiles (M = 131072)
+    (64, 32, 64, 64, "bf16"),
 ])
 def test_vectors_shapes(lib, d, K, N, B, e_dtype):
     print(f"vectors d={d} K={K} N={N} B={B} {e_dtype}", flush=True)
@@ -79,6 +84,7 @@ def test_vectors_identity_weights(lib):
 @pytest.mark.parametrize("N,B,K,d,anchor", [
     (1, 2, 1, 16, False), (2, 3, 3, 48, True), (4, 16, 16, 256, True), (2, 16, 32, 512, False),
     (1, 5, 64, 1024, True), (3, 1, 8, 64, True), (2, 4, 17, 144, True),
+    (2, 3, 40, 80, True), (1, 3, 64, 1008, False), (3, 4, 33, 208, False),
 ])
 def test_pair_scores_shapes(lib, N, B, K, d, anchor):
     print(f"pairs N={N} B={B} K={K} d={d} anchor={anchor}", flush=True)

@@ -32,6 +32,8 @@ def _walk(lib, S, S0, logp, ids, lam=0.0):
     (1, 1, 1, False, 0.0, False), (3, 2, 2, True, 0.0, True), (16, 16, 16, False, 0.0, True),
     (7, 16, 32, True, 0.0, False), (5, 9, 64, True, 0.0, True), (4, 30, 64, False, 0.0, False),
     (8, 16, 8, True, 1.0, False), (2, 6, 5, False, -0.5, True),
+    # several table segments per request (slots per segment: 2048 // K)
+    (2, 100, 64, True, 0.0, True), (1, 1500, 3, False, 0.0, True), (3, 70, 33, False, 1.0, False),
 ])
 def test_walk_random(lib, N, B, K, anchor, lam, coarse):
     print(f"walk N={N} B={B} K={K} anchor={anchor} lam={lam}", flush=True)
