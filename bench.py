@@ -2,11 +2,14 @@
 """Benchmark of the LiLiCorr draft-correlation hot path on one MI355X.
 
 One step = the whole path over one batch of synthetic input, on one stream:
-    lilicorr_topk -> lilicorr_candidate_vectors -> lilicorr_pair_scores -> lilicorr_greedy_walk
+    lilicorr_topk -> lilicorr_score_walk (candidate vectors, pair scores and greedy walk in one
+    pass, the in/out vectors kept on chip)
 for the headline workload (N = 64 requests, B = 16 slots, K = 16 candidates, V = 151936,
 d = 256, bf16 logits). The metric is scored draft blocks per second (N blocks per step). Logits
 rotate over four resident copies (1.2 GB, above the 256 MB Infinity Cache) so every step streams
 its logits from HBM; the embedding table and packed weights stay resident, as served weights do.
+The same steps through the four separate calls (topk -> candidate_vectors -> pair_scores ->
+greedy_walk, in/out vectors through HBM) are timed too and reported beside it.
 
 Printed: one JSON line with the step throughput, a roofline entry for the dominant kernel (the
 logits pass, timed with HIP events around each of its launches on the launch stream), the
@@ -148,28 +151,44 @@ def main():
     choice = torch.empty_like(draft)
     logq = torch.empty(N, B, dtype=torch.float32, device=dev)
 
+    ws_fused = L.score_walk_workspace(N, B, K)
+
     def step(i, ev=None):
         if ev is not None:
             ev[0].record()
         L.topk(logits_list[i % ROTATE], K, out=(ids, logp), workspace=ws)
         if ev is not None:
             ev[1].record()
+        L.score_walk(ids, logp, E, packed, None, L.SIGMA, 0.0, out=(draft, choice, logq),
+                     workspace=ws_fused)
+
+    def step_separate(i):
+        L.topk(logits_list[i % ROTATE], K, out=(ids, logp), workspace=ws)
         L.candidate_vectors(ids, E, packed, out=(in_vec, out_vec))
         L.pair_scores(in_vec, out_vec, None, L.SIGMA, out=(S, None))
         L.greedy_walk(S, None, logp, ids, 0.0, out=(draft, choice, logq))
 
+    def timed(fn, steps, evs=None):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            if evs is None:
+                fn(i)
+            else:
+                fn(i, evs[i])
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
     for i in range(args.warmup):
         step(i)
+        step_separate(i)
     torch.cuda.synchronize()
+    sep_elapsed = timed(step_separate, args.steps)
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(i, evs[i])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    print(f"[bench] timed {args.steps} steps in {elapsed:.4f} s", file=sys.stderr, flush=True)
+    elapsed = timed(step, args.steps, evs)
+    print(f"[bench] timed {args.steps} steps in {elapsed:.4f} s (separate calls: "
+          f"{sep_elapsed:.4f} s)", file=sys.stderr, flush=True)
 
     ms_per_step = elapsed / args.steps * 1e3
     value = N * args.steps / elapsed
@@ -195,12 +214,16 @@ def main():
         "config": {"workload": "headline: N=64 requests, B=16 slots, K=16, V=151936, d=256, "
                                "bf16 logits (3 entropy tiers, 1% exact ties), bf16 embeddings, "
                                "fp32 weights; no anchor; sigma=8",
+                   "path": "lilicorr_topk -> lilicorr_score_walk",
                    "N": N, "B": B, "K": K, "V": V, "d": d, "logits_dtype": "bf16",
                    "logits_rotation": ROTATE},
         "roofline": {"bound": "hbm", "kernel": "topk_lse_kernel", "achieved": achieved,
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
                      "traffic": traffic, "avg_launch_us": topk_s * 1e6,
                      "algorithmic_bytes_per_launch": algo_bytes},
+        "separate_calls": {"path": "topk -> candidate_vectors -> pair_scores -> greedy_walk",
+                           "ms_per_step": sep_elapsed / args.steps * 1e3,
+                           "value": N * args.steps / sep_elapsed},
     }
 
     if not args.no_stress:

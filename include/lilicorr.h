@@ -131,6 +131,34 @@ lilicorr_status lilicorr_greedy_walk(const float *S, const float *S0, const floa
                                      float logp_weight, int32_t *draft, int32_t *choice,
                                      float *logq, hipStream_t stream);
 
+/*
+ * Steps 2-4 in one pass (Sec. 3.5: all pair matrices in one batched pass, then the greedy walk;
+ * the implementation appendix serves matching and selection as a single replay): the draft,
+ * choice and logq that lilicorr_candidate_vectors -> lilicorr_pair_scores -> lilicorr_greedy_walk
+ * give on the same inputs, without writing the in/out vectors to memory.
+ *   ids, logp      [N][B][K] from step 1.
+ *   E, e_dtype, V, d, packed_w   as for lilicorr_candidate_vectors (bf16 E only, d <= 256).
+ *   anchor_out     [N][d] fp32 or NULL, as for lilicorr_pair_scores.
+ *   sigma          cosine scale of Eq. (pair); logp_weight as for lilicorr_greedy_walk.
+ *   S, S0          optional outputs, NULL to skip: the pair scores as lilicorr_pair_scores defines
+ *                  them (S0 only with anchor_out).
+ *   draft, choice, logq   as for lilicorr_greedy_walk (choice and logq may be NULL).
+ *   workspace      lilicorr_score_walk_workspace_bytes(N, B, K) bytes of device memory, owned by
+ *                  the caller, zero-filled once before its first use; every call leaves it ready
+ *                  for the next (its counters back at zero). Calls sharing a workspace must not
+ *                  overlap in time.
+ * Limits: K <= 64, 1 + (B-1) K <= 16384, bf16 E, d a multiple of 16 and at most 256
+ * (LILICORR_ERR_UNSUPPORTED otherwise; LILICORR_ERR_WORKSPACE if the workspace is too small).
+ * lilicorr_score_walk_workspace_bytes returns 0 outside these limits.
+ */
+size_t lilicorr_score_walk_workspace_bytes(int64_t N, int64_t B, int K);
+lilicorr_status lilicorr_score_walk(const int32_t *ids, const float *logp, const void *E,
+                                    lilicorr_dtype e_dtype, int64_t V, int d,
+                                    const void *packed_w, const float *anchor_out, int64_t N,
+                                    int64_t B, int K, float sigma, float logp_weight, float *S,
+                                    float *S0, int32_t *draft, int32_t *choice, float *logq,
+                                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char *lilicorr_status_string(lilicorr_status s);
 

@@ -7,6 +7,7 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
   lilicorr_candidate_vectors  ids, E -> in_vec, out_vec [N,B,K,d]       (Sec. 3.2 unit-norm heads)
   lilicorr_pair_scores        in/out -> S [N,B-1,K,K] (+ S0 [N,K])      (Eq. pair)
   lilicorr_greedy_walk        S, S0, logp, ids -> draft, choice, logq   (Sec. 3.5, Eq. localar)
+  lilicorr_score_walk         ids, logp, E -> draft, choice, logq       (steps 2-4 in one pass)
 
 This module only marshals arguments: torch supplies device memory and the current HIP stream,
 and every step of the path runs in the library's kernels. There is no fallback: if the library
@@ -23,8 +24,10 @@ __all__ = [
     "LIB_PATH", "load_library", "LilicorrError", "SIGMA",
     "lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
-    "lilicorr_greedy_walk", "lilicorr_status_string",
-    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "draft_block",
+    "lilicorr_greedy_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+    "lilicorr_status_string",
+    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "score_walk",
+    "draft_block",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblilicorr.so")
@@ -57,6 +60,9 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_candidate_vectors": ([P, P, I, I64, I, P, I64, I64, I, P, P, P], I),
         "lilicorr_pair_scores": ([P, P, P, I64, I64, I, I, F, P, P, P], I),
         "lilicorr_greedy_walk": ([P, P, P, P, I64, I64, I, F, P, P, P, P], I),
+        "lilicorr_score_walk_workspace_bytes": ([I64, I64, I], SZ),
+        "lilicorr_score_walk": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, SZ,
+                                 P], I),
         "lilicorr_status_string": ([I], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -110,6 +116,17 @@ def lilicorr_pair_scores(in_vec, out_vec, anchor_out, N, B, K, d, sigma, S, S0, 
 def lilicorr_greedy_walk(S, S0, logp, ids, N, B, K, logp_weight, draft, choice, logq, stream):
     return _call("lilicorr_greedy_walk", S, S0, logp, ids, N, B, K, logp_weight, draft, choice,
                  logq, stream)
+
+
+def lilicorr_score_walk_workspace_bytes(N: int, B: int, K: int) -> int:
+    return int(load_library().lilicorr_score_walk_workspace_bytes(N, B, K))
+
+
+def lilicorr_score_walk(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K, sigma,
+                        logp_weight, S, S0, draft, choice, logq, workspace, workspace_bytes, stream):
+    return _call("lilicorr_score_walk", ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
+                 K, sigma, logp_weight, S, S0, draft, choice, logq, workspace, workspace_bytes,
+                 stream)
 
 
 # ---- torch conveniences (marshalling only) -----------------------------------------------------
@@ -208,6 +225,45 @@ def greedy_walk(S: torch.Tensor, S0, logp: torch.Tensor, ids: torch.Tensor,
                          _dev(ids, "ids", (torch.int32,)), N, B, K, float(logp_weight),
                          _dev(draft, "draft", (torch.int32,)), _dev(choice, "choice", (torch.int32,)),
                          _dev(logq, "logq", (torch.float32,)), _stream())
+    return draft, choice, logq
+
+
+def score_walk_workspace(N: int, B: int, K: int, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace for score_walk (the library keeps it zeroed between calls)."""
+    need = lilicorr_score_walk_workspace_bytes(N, B, K)
+    if need == 0:
+        raise LilicorrError(f"score_walk does not support N={N}, B={B}, K={K}")
+    return torch.zeros(need, dtype=torch.uint8, device=device)
+
+
+def score_walk(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor, packed: torch.Tensor,
+               anchor_out=None, sigma: float = SIGMA, logp_weight: float = 0.0, *,
+               scores: bool = False, out=None, workspace=None):
+    """Steps 2-4 in one pass -> (draft, choice, logq[, S, S0 when scores=True])."""
+    N, B, K = ids.shape
+    V, d = E.shape
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.float32, device=dev))
+    draft, choice, logq = out
+    S = S0 = None
+    if scores:
+        S = torch.empty(N, max(B - 1, 0), K, K, dtype=torch.float32, device=dev)
+        S0 = torch.empty(N, K, dtype=torch.float32, device=dev) if anchor_out is not None else None
+    if workspace is None:
+        workspace = score_walk_workspace(N, B, K, dev)
+    lilicorr_score_walk(_dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)),
+                        _dev(E, "E", (torch.bfloat16, torch.float32)), _dtype_code(E), V, d,
+                        _dev(packed, "packed"), _dev(anchor_out, "anchor_out", (torch.float32,)),
+                        N, B, K, float(sigma), float(logp_weight),
+                        _dev(S, "S", (torch.float32,)) if S is not None and B > 1 else None,
+                        _dev(S0, "S0", (torch.float32,)), _dev(draft, "draft", (torch.int32,)),
+                        _dev(choice, "choice", (torch.int32,)), _dev(logq, "logq", (torch.float32,)),
+                        _dev(workspace, "workspace"), workspace.numel(), _stream())
+    if scores:
+        return draft, choice, logq, S, S0
     return draft, choice, logq
 
 

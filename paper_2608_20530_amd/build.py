@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblilicorr.so")
-SOURCES = ["topk.hip", "vectors.hip", "pairs.hip", "walk.hip", "status.hip"]
+SOURCES = ["topk.hip", "vectors.hip", "pairs.hip", "walk.hip", "fused.hip", "status.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -211,4 +211,45 @@ __device__ __forceinline__ float sort_desc64(float v) {
   return v;
 }
 
+// ---- one row of the walk -----------------------------------------------------------------------
+// all-reduce over aligned groups of G lanes; every lane of a group receives the group's result
+template <typename Op>
+__device__ __forceinline__ float dpp_allreduce16(float v, Op op) {
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false)));   // quad_perm 1,0,3,2
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xf, 0xf, false)));   // quad_perm 2,3,0,1
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xf, 0xf, false)));  // row_half_mirror
+  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xf, 0xf, false)));  // row_mirror
+  return v;
+}
+
+template <int G, typename Op>
+__device__ __forceinline__ float group_allreduce(float v, Op op) {
+  v = dpp_allreduce16(v, op);
+  if (G >= 32) v = op(v, __shfl_xor(v, 16, kWave));
+  if (G >= 64) v = op(v, __shfl_xor(v, 32, kWave));
+  return v;
+}
+
+// One row of the walk's transition table, resolved by an aligned group of G lanes (lane j of the
+// group holds z_j; lanes with live == false hold no candidate): the lowest j attaining max z
+// (0 if none does, which only NaN scores cause) and the local log-likelihood
+// -log sum_j exp(z_j - max z) of Eq. (localar), both in fp32. Every lane of the wave must call it.
+template <int G>
+__device__ __forceinline__ void resolve_row(float z, bool live, int& arg, float& lq) {
+  const int gshift = (lane_id() / G) * G;  // first ballot bit of this lane's group
+  const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
+  const float m = group_allreduce<G>(live ? z : -__builtin_inff(),
+                                     [](float a, float b) { return fmaxf(a, b); });
+  const uint64_t hits = (__ballot(live && z == m) >> gshift) & gmask;
+  arg = hits ? __ffsll((long long)hits) - 1 : 0;
+  const float s = group_allreduce<G>(live ? expf(z - m) : 0.f,
+                                     [](float a, float b) { return a + b; });
+  lq = -logf(s);
+}
+
+// table entry: low 32 bits the argmax, high 32 bits the fp32 local log-likelihood
+__device__ __forceinline__ uint64_t table_entry(int arg, float lq) {
+  return (uint64_t)(uint32_t)arg | ((uint64_t)__float_as_uint(lq) << 32);
+}
+
 }  // namespace lilicorr

@@ -1,0 +1,356 @@
+// Steps 2-4 of the path in one kernel: candidate vectors (the in/out heads' stand-in u = E[id] W,
+// Sec. 3.2), batched pair scores sigma * cos (Eq. pair, one matrix per adjacent slot pair,
+// Sec. 3.5) and the greedy walk with its local log-likelihoods (Sec. 3.5, Eq. localar). The
+// paper's serving path runs matching and selection as one replay; here the in/out vectors never
+// leave the compute unit that made them.
+//
+// A workgroup owns up to P = 64 / K consecutive slot pairs (t, t+1) of one request:
+//  1. it gathers the embedding rows of the out side (slots t0 .. t0+P-1) and of the in side
+//     (slots t0+1 .. t0+P) into one bf16 LDS tile, 64 rows per side;
+//  2. half of its waves project the out rows onto W_out and half the in rows onto W_in on the bf16
+//     matrix cores (exact three-term weight split), each wave owning four 16-column blocks;
+//  3. the raw projections u (fp32) replace the tile in LDS, with their squared norms;
+//  4. every pair's K x K block is contracted on the fp32 matrix cores from LDS and scaled:
+//     S = sigma * <u_o, u_i> / (||u_o|| ||u_i||) (a zero vector scores 0);
+//  5. every row (slot t+1, previous choice p) of the walk's transition table is resolved from S:
+//     argmax (lowest index on ties) and -log sum exp(z - max z), and written to the workspace;
+//  6. the workgroup takes a ticket; the last one of its request to finish stages the request's
+//     table in LDS, follows it slot by slot and writes draft, choice and logq.
+// The anchor pair (when given) has a workgroup of its own: in rows of slot 0 against anchor_out.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "common.hpp"
+#include "lilicorr.h"
+#include "projection.hpp"
+
+namespace lilicorr {
+namespace {
+
+constexpr int kSideRows = 64;                // candidate rows per side per workgroup
+constexpr int kSideRm = kSideRows / 16;      // 16-row blocks per side
+constexpr int kFusedMaxD = 256;              // the fp32 projections of both sides fit in LDS
+constexpr int64_t kMaxTableRows = 16384;     // a request's table is staged in LDS at the end
+constexpr size_t kCounterBytes = 256;        // counters are padded to this alignment
+
+struct FusedPlan {
+  int P;             // slot pairs per workgroup
+  int groups;        // pair groups per request
+  int wg;            // workgroups per request (pair groups + the anchor's)
+  int ws;            // waves per side
+  int astride;       // bf16 elements per gathered row in LDS
+  int vstride;       // floats per projected row in LDS
+  int64_t rows;      // transition-table rows per request: 1 + (B-1) K
+  size_t x_bytes;    // shared region: gathered tile, then projections, then (last) the table
+  size_t lds_bytes;  // total dynamic LDS
+};
+
+inline FusedPlan fused_plan(int64_t B, int K, int d) {
+  FusedPlan p;
+  const VecGeom g = vec_geom(d);
+  p.P = kSideRows / K;
+  const int64_t pairs = B - 1;
+  p.groups = pairs > 0 ? (int)((pairs + p.P - 1) / p.P) : 1;
+  p.wg = p.groups;  // the anchor workgroup is added by the caller when present
+  p.ws = g.waves;
+  p.astride = g.dkp * 32 + 8;
+  p.vstride = d + 4;
+  p.rows = 1 + (B - 1) * K;
+  const size_t a_bytes = (size_t)2 * kSideRows * p.astride * 2;
+  const size_t v_bytes = (size_t)2 * kSideRows * p.vstride * 4;
+  const size_t t_bytes = (size_t)p.rows * 8 + (size_t)B * 8;
+  p.x_bytes = a_bytes > v_bytes ? a_bytes : v_bytes;
+  if (t_bytes > p.x_bytes) p.x_bytes = t_bytes;
+  p.x_bytes = (p.x_bytes + 15) / 16 * 16;
+  p.lds_bytes = p.x_bytes + (size_t)2 * p.ws * kSideRows * 4  // per-wave partial norms
+                + (size_t)2 * kSideRows * 4                   // row squared norms
+                + (size_t)2 * kSideRows * 4                   // row token ids
+                + (size_t)p.P * K * K * 4                     // this workgroup's scores
+                + 16;                                         // ticket flag
+  return p;
+}
+
+inline size_t fused_workspace_bytes(int64_t N, int64_t B, int K) {
+  const size_t counters = ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
+  return counters + (size_t)N * (size_t)(1 + (B - 1) * K) * 8;
+}
+
+template <int G>
+__global__ __launch_bounds__(512) void score_walk_kernel(
+    const int32_t* __restrict__ ids, const float* __restrict__ logp,
+    const uint16_t* __restrict__ E, int64_t V, int d, const unsigned char* __restrict__ frags,
+    int nbp, int dkp, const float* __restrict__ anchor_out, int64_t B, int K, float sigma,
+    float lambda, FusedPlan plan, float* __restrict__ S, float* __restrict__ S0,
+    int32_t* __restrict__ draft, int32_t* __restrict__ choice, float* __restrict__ logq,
+    uint32_t* __restrict__ counters, uint64_t* __restrict__ table) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [128][astride] gathered rows
+  float* Vf = reinterpret_cast<float*>(smem);       // [128][vstride] projections (after A)
+  uint64_t* tbl = reinterpret_cast<uint64_t*>(smem);  // [rows] the request's table (last wg)
+  float* ssw = reinterpret_cast<float*>(smem + plan.x_bytes);  // [2][ws][64]
+  float* nrm = ssw + 2 * plan.ws * kSideRows;                   // [128]
+  int32_t* rid = reinterpret_cast<int32_t*>(nrm + 2 * kSideRows);  // [128]
+  float* sbuf = reinterpret_cast<float*>(rid + 2 * kSideRows);     // [P][K][K]
+  int* flag = reinterpret_cast<int*>(sbuf + plan.P * K * K);
+
+  const int tid = threadIdx.x;
+  const int nthreads = blockDim.x;
+  const int nwaves = nthreads / kWave;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
+  const int64_t n = blockIdx.x / plan.wg;
+  const int g = (int)(blockIdx.x % plan.wg);
+  const bool anchor_wg = anchor_out != nullptr && g == plan.groups;
+  const int t0 = anchor_wg ? 0 : g * plan.P;
+  const int npair = anchor_wg ? 0 : (int)((B - 1 - t0) < plan.P ? (B - 1 - t0) : plan.P);
+  const int n_out = npair * K;                 // out rows: slots t0 .. t0+npair-1
+  const int n_in = anchor_wg ? K : npair * K;  // in rows: slots t0+1 .. (slot 0 for the anchor)
+  const int in_slot0 = anchor_wg ? 0 : t0 + 1;
+  const int dpad = dkp * 32;
+  const bool use_lp = lambda != 0.f;
+  const float* lpn = logp + n * B * K;
+
+  // ---- 1. gather ------------------------------------------------------------------------------
+  // wave w: local side w / ws (0: out rows on W_out, packed side 1; 1: in rows on W_in, side 0)
+  const int lside = wave / plan.ws, cg = wave % plan.ws;
+  const int side_rows = lside == 0 ? n_out : n_in;
+  const size_t slice = (size_t)nbp * 1024;
+  const unsigned char* wf = frags + (size_t)(lside == 0 ? 1 : 0) * dkp * 3 * slice +
+                            (size_t)cg * kNbPerWave * 1024 + lane * 16;
+  BFrag b0;
+  if (side_rows > 0) load_bfrag(b0, wf, slice, 0);  // in flight during the gather
+  for (int r = tid; r < 2 * kSideRows; r += nthreads) {
+    const int rs = r / kSideRows, lr = r % kSideRows;
+    int32_t id = -1;
+    if (lr < (rs == 0 ? n_out : n_in)) {
+      const int slot = (rs == 0 ? t0 : in_slot0) + lr / K;
+      id = ids[(n * B + slot) * K + lr % K];
+      if (id < 0 || id >= V) id = -1;  // outside the table: a zero row
+    }
+    rid[r] = id;
+  }
+  __syncthreads();
+  gather_rows(A, plan.astride, 2 * kSideRows, rid, E, d, dpad, tid, nthreads);
+  __syncthreads();
+
+  // ---- 2. projection --------------------------------------------------------------------------
+  f32x4 acc[kSideRm][kNbPerWave];
+  if (side_rows > 0) {
+    project_tile<kSideRm>(acc, b0, A + lside * kSideRows * plan.astride, plan.astride, wf, slice,
+                          dkp, lane);
+    row_sumsq<kSideRm>(acc, ssw + (lside * plan.ws + cg) * kSideRows, lane);
+  }
+  __syncthreads();  // every wave is done reading the gathered tile
+
+  // ---- 3. projections and squared norms into LDS -------------------------------------------
+  for (int r = tid; r < 2 * kSideRows; r += nthreads) {
+    const int rs = r / kSideRows, lr = r % kSideRows;
+    float t = 0.f;
+    if (lr < (rs == 0 ? n_out : n_in))
+      for (int c = 0; c < plan.ws; ++c) t += ssw[(rs * plan.ws + c) * kSideRows + lr];
+    nrm[r] = t;
+  }
+  if (side_rows > 0) {
+    const int col0 = cg * kNbPerWave * 16 + (lane & 15);
+#pragma unroll
+    for (int mb = 0; mb < kSideRm; ++mb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = lside * kSideRows + mb * 16 + (lane >> 4) * 4 + i;
+#pragma unroll
+        for (int nb = 0; nb < kNbPerWave; ++nb)
+          if (col0 + nb * 16 < d) Vf[row * plan.vstride + col0 + nb * 16] = acc[mb][nb][i];
+      }
+  }
+  __syncthreads();
+
+  // ---- 4. scores --------------------------------------------------------------------------------
+  const int r16 = lane & 15, q = lane >> 4;
+  if (!anchor_wg) {
+    const int nbk = (K + 15) / 16;
+    const int ntiles = npair * nbk * nbk;
+    for (int tile = wave; tile < ntiles; tile += nwaves) {
+      const int p = tile / (nbk * nbk), bl = (tile / nbk) % nbk, br = tile % nbk;
+      const int orow = p * K + bl * 16 + r16, irow = kSideRows + p * K + br * 16 + r16;
+      const bool ov = bl * 16 + r16 < K, iv = br * 16 + r16 < K;
+      const float* po = Vf + orow * plan.vstride + 4 * q;
+      const float* pi = Vf + irow * plan.vstride + 4 * q;
+      f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
+      // MFMA step (s, e) contracts column 16 s + 4 q + e of both sides
+      for (int s = 0; s < d; s += 16) {
+        const f32x4 a = ov ? *reinterpret_cast<const f32x4*>(po + s) : f32x4{0.f, 0.f, 0.f, 0.f};
+        const f32x4 b = iv ? *reinterpret_cast<const f32x4*>(pi + s) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
+      }
+      // lane (r16, q) holds rows 4 q + i, column r16 of the tile
+      const int kk = br * 16 + r16;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = bl * 16 + 4 * q + i;
+        if (k < K && kk < K) {
+          const float den = sqrtf(nrm[p * K + k]) * sqrtf(nrm[kSideRows + p * K + kk]);
+          sbuf[(p * K + k) * K + kk] = den > 0.f ? sigma * (c[i] / den) : 0.f;
+        }
+      }
+    }
+  } else {
+    // anchor pair: S0[k'] = sigma * cos(anchor_out[n], in vector k' of slot 0)
+    const float* a = anchor_out + n * d;
+    for (int kk = tid; kk < K; kk += nthreads) {
+      float dot = 0.f, na = 0.f;
+      for (int j = 0; j < d; ++j) {
+        const float x = a[j];
+        dot = fmaf(x, Vf[(kSideRows + kk) * plan.vstride + j], dot);
+        na = fmaf(x, x, na);
+      }
+      const float den = sqrtf(na) * sqrtf(nrm[kSideRows + kk]);
+      sbuf[kk] = den > 0.f ? sigma * (dot / den) : 0.f;
+    }
+  }
+  __syncthreads();
+
+  // ---- 5. transition-table rows (and the optional score outputs) -----------------------------
+  {
+    // rows of this workgroup: (slot t0+p+1, previous choice k) for p < npair, k < K; plus row 0
+    // (slot 0) in the anchor workgroup, or in group 0 when there is no anchor
+    const bool has_row0 = anchor_wg || (anchor_out == nullptr && g == 0);
+    const int nrows = npair * K + (has_row0 ? 1 : 0);
+    const int j = tid % G;
+    const int ngroups = nthreads / G;
+    const bool live = j < K;
+    for (int base = 0; base < nrows; base += ngroups) {
+      const int lr = base + tid / G;  // local row: 0 .. npair*K-1 pair rows, then row 0
+      float z = 0.f;
+      int64_t grow = -1;
+      if (lr < nrows && live) {
+        if (lr < npair * K) {
+          const int p = lr / K;
+          z = sbuf[lr * K + j];
+          if (use_lp) z = fmaf(lambda, lpn[(t0 + p + 1) * K + j], z);
+        } else {
+          z = anchor_wg ? sbuf[j] : 0.f;
+          if (use_lp) z = fmaf(lambda, lpn[j], z);
+        }
+      }
+      if (lr < nrows) grow = lr < npair * K ? 1 + (int64_t)t0 * K + lr : 0;
+      int arg;
+      float lq;
+      resolve_row<G>(z, live, arg, lq);
+      if (j == 0 && grow >= 0) table[n * plan.rows + grow] = table_entry(arg, lq);
+    }
+    if (S && npair > 0) {
+      float* dst = S + ((n * (B - 1) + t0) * K) * (int64_t)K;
+      for (int i = tid; i < npair * K * K; i += nthreads) dst[i] = sbuf[i];
+    }
+    if (anchor_wg && S0)
+      for (int i = tid; i < K; i += nthreads) S0[n * K + i] = sbuf[i];
+  }
+
+  // ---- 6. ticket; the request's last workgroup walks -----------------------------------------
+  // The workgroup barrier completes every wave's stores; one thread then releases them to the
+  // whole device and takes the ticket. Only the request's last workgroup acquires (a device-wide
+  // fence in every thread, or an acquire in every workgroup, would invalidate cached weights
+  // under the other workgroups still running: measured 2.7x slower).
+  __syncthreads();
+  if (tid == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    const uint32_t done =
+        __hip_atomic_fetch_add(&counters[n], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = done == (uint32_t)(plan.wg - 1);
+    if (*flag) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+  __syncthreads();
+  if (!*flag) return;
+  for (int64_t i = tid; i < plan.rows; i += nthreads) tbl[i] = table[n * plan.rows + i];
+  int32_t* ch = reinterpret_cast<int32_t*>(tbl + plan.rows);  // [B]
+  float* lq_t = reinterpret_cast<float*>(ch + B);             // [B]
+  __syncthreads();
+  if (tid == 0) {
+    int c = 0;
+    for (int64_t t = 0; t < B; ++t) {
+      const uint64_t e = tbl[t == 0 ? 0 : 1 + (t - 1) * K + c];
+      c = (int)(uint32_t)e;
+      ch[t] = c;
+      lq_t[t] = __uint_as_float((uint32_t)(e >> 32));
+    }
+    counters[n] = 0u;  // ready for the next call (visible to it at the kernel boundary)
+  }
+  __syncthreads();
+  for (int64_t t = tid; t < B; t += nthreads) {
+    const int ct = ch[t];
+    draft[n * B + t] = ids[(n * B + t) * K + ct];
+    if (choice) choice[n * B + t] = ct;
+    if (logq) logq[n * B + t] = lq_t[t];
+  }
+}
+
+template <int G>
+void launch_score_walk(const FusedPlan& plan, int64_t N, hipStream_t stream, const int32_t* ids,
+                       const float* logp, const uint16_t* E, int64_t V, int d,
+                       const unsigned char* frags, int nbp, int dkp, const float* anchor_out,
+                       int64_t B, int K, float sigma, float lambda, float* S, float* S0,
+                       int32_t* draft, int32_t* choice, float* logq, uint32_t* counters,
+                       uint64_t* table) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(score_walk_kernel<G>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  (void)attr;
+  hipLaunchKernelGGL(score_walk_kernel<G>, dim3((unsigned)(N * plan.wg)), dim3(2 * plan.ws * kWave),
+                     plan.lds_bytes, stream, ids, logp, E, V, d, frags, nbp, dkp, anchor_out, B, K,
+                     sigma, lambda, plan, S, S0, draft, choice, logq, counters, table);
+}
+
+}  // namespace
+}  // namespace lilicorr
+
+using namespace lilicorr;
+
+extern "C" size_t lilicorr_score_walk_workspace_bytes(int64_t N, int64_t B, int K) {
+  if (N < 1 || B < 1 || K < 1 || K > 64) return 0;
+  if (1 + (B - 1) * (int64_t)K > kMaxTableRows) return 0;
+  return fused_workspace_bytes(N, B, K);
+}
+
+extern "C" lilicorr_status lilicorr_score_walk(
+    const int32_t* ids, const float* logp, const void* E, lilicorr_dtype e_dtype, int64_t V, int d,
+    const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
+    float logp_weight, float* S, float* S0, int32_t* draft, int32_t* choice, float* logq,
+    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!ids || !logp || !E || !packed_w || !draft || !workspace) return LILICORR_ERR_INVALID_ARG;
+  if (e_dtype != LILICORR_F32 && e_dtype != LILICORR_BF16) return LILICORR_ERR_INVALID_ARG;
+  if (N < 1 || B < 1 || K < 1 || V < 1 || d < 1) return LILICORR_ERR_INVALID_ARG;
+  if (!isfinite(sigma) || !isfinite(logp_weight)) return LILICORR_ERR_INVALID_ARG;
+  if (e_dtype != LILICORR_BF16) return LILICORR_ERR_UNSUPPORTED;
+  if (d % 16 != 0 || d > kFusedMaxD || K > 64 || V >= ((int64_t)1 << 31))
+    return LILICORR_ERR_UNSUPPORTED;
+  if (B > kMaxTableRows || 1 + (B - 1) * (int64_t)K > kMaxTableRows) return LILICORR_ERR_UNSUPPORTED;
+  if (!aligned16(ids) || !aligned16(logp) || !aligned16(E) || !aligned16(packed_w) ||
+      !aligned16(draft) || !aligned16(workspace) || (anchor_out && !aligned16(anchor_out)) ||
+      (S && !aligned16(S)) || (S0 && !aligned16(S0)) || (choice && !aligned16(choice)) ||
+      (logq && !aligned16(logq)))
+    return LILICORR_ERR_ALIGNMENT;
+  if (workspace_bytes < fused_workspace_bytes(N, B, K)) return LILICORR_ERR_WORKSPACE;
+  FusedPlan plan = fused_plan(B, K, d);
+  if (anchor_out) plan.wg += 1;
+  if (N > 0x7fffffffll / plan.wg) return LILICORR_ERR_UNSUPPORTED;
+  if (plan.lds_bytes > 160 * 1024) return LILICORR_ERR_UNSUPPORTED;
+  const VecGeom g = vec_geom(d);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
+  uint64_t* table = reinterpret_cast<uint64_t*>(
+      ws + ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes);
+  const uint16_t* e16 = static_cast<const uint16_t*>(E);
+  const unsigned char* frags = static_cast<const unsigned char*>(packed_w);
+  if (K <= 16)
+    launch_score_walk<16>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp, anchor_out,
+                          B, K, sigma, logp_weight, S, S0, draft, choice, logq, counters, table);
+  else if (K <= 32)
+    launch_score_walk<32>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp, anchor_out,
+                          B, K, sigma, logp_weight, S, S0, draft, choice, logq, counters, table);
+  else
+    launch_score_walk<64>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp, anchor_out,
+                          B, K, sigma, logp_weight, S, S0, draft, choice, logq, counters, table);
+  return launch_status();
+}

@@ -1,0 +1,168 @@
+// Device helpers of the candidate projection u = E[id] W on the bf16 matrix cores, shared by the
+// candidate-vector kernel and the fused scoring kernel.
+//
+// Every fp32 weight is split exactly into three bf16 terms (hi + mid + lo == w); E is bf16, so each
+// bf16 x bf16 product is exact in fp32 and fp32 accumulation gives fp32-grade results.
+//
+// Packed weight layout (written by lilicorr_pack_weights):
+//   [side 2][k-block dkp][term 3][column block nbp][lane 64][8 bf16]: v_mfma_f32_16x16x32_bf16
+//     B fragments; lane l of block (kb, nb) holds W[kb*32 + (l/16)*8 + i][nb*16 + l%16], i = 0..7
+//     (0 for rows or columns at or beyond d)
+//   followed by [side 2][d][d] fp32 copies (used by the fp32-embedding kernel)
+// Side 0 is W_in, side 1 is W_out. nbp is d/16 rounded up to whole wave column groups and dkp is
+// the number of 32-deep k-blocks rounded up to even, so the MFMA loop never branches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace lilicorr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kNbPerWave = 4;  // 16-column blocks owned by each wave
+
+struct VecGeom {
+  int d16;    // 16-column blocks of the output
+  int nbp;    // d16 rounded up to whole waves (kNbPerWave blocks each)
+  int dk;     // 32-deep k-blocks of the contraction
+  int dkp;    // dk rounded up to even (the MFMA loop handles two k-blocks per trip)
+  int waves;  // waves per side: one per kNbPerWave column blocks
+  int rm;     // 16-row blocks per workgroup of the candidate-vector kernel
+};
+
+// rm: up to d = 512, 128-row tiles once there are enough of them to give every compute unit
+// several (a workgroup's phases, gather -> MFMA -> store, then overlap with other workgroups'),
+// else 64-row tiles, which put two workgroups on each compute unit; 32-row tiles above d = 512
+inline VecGeom vec_geom(int d, int64_t M = 0) {
+  VecGeom g;
+  g.d16 = d / 16;
+  g.nbp = (g.d16 + kNbPerWave - 1) / kNbPerWave * kNbPerWave;
+  g.dk = (d + 31) / 32;
+  g.dkp = (g.dk + 1) / 2 * 2;
+  g.waves = g.nbp / kNbPerWave;
+  g.rm = d > 512 ? 2 : ((M + 127) / 128 * 2 >= 2048 ? 8 : 4);
+  return g;
+}
+
+inline size_t frag_bytes(int d) {
+  VecGeom g = vec_geom(d);
+  return (size_t)2 * g.dkp * 3 * g.nbp * 1024;
+}
+
+inline size_t packed_bytes(int d) { return frag_bytes(d) + (size_t)2 * d * d * sizeof(float); }
+
+typedef u32x4 BFrag[kNbPerWave][3];
+
+// B fragments of k-block kb for a wave's four column blocks, three terms each; wf points at the
+// wave's first column block (plus lane * 16) in k-block 0, term 0 of its side
+__device__ __forceinline__ void load_bfrag(BFrag& dst, const unsigned char* wf, size_t slice,
+                                           int kb) {
+  const unsigned char* p = wf + (size_t)kb * 3 * slice;
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int nb = 0; nb < kNbPerWave; ++nb)
+      dst[nb][t] = *reinterpret_cast<const u32x4*>(p + t * slice + nb * 1024);
+}
+
+// acc[mb][nb] += A[rows of block mb][k-block kb] x B[k-block kb][column block nb], all three
+// terms; the term loop is outermost so consecutive MFMAs never feed each other
+template <int RM>
+__device__ __forceinline__ void mfma_kblock(f32x4 (&acc)[RM][kNbPerWave], const BFrag& b,
+                                            const uint16_t* A, int astride, int kb, int lane) {
+  bf16x8 a[RM];
+  const int kcol = kb * 32 + (lane >> 4) * 8;
+#pragma unroll
+  for (int mb = 0; mb < RM; ++mb)
+    a[mb] = __builtin_bit_cast(
+        bf16x8, *reinterpret_cast<const u32x4*>(A + (mb * 16 + (lane & 15)) * astride + kcol));
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int mb = 0; mb < RM; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kNbPerWave; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            a[mb], __builtin_bit_cast(bf16x8, b[nb][t]), acc[mb][nb], 0, 0, 0);
+}
+
+// The whole contraction of a wave's RM row blocks x four column blocks. b0 must already hold
+// k-block 0 (so its loads can overlap whatever precedes). Two k-blocks per trip through two
+// register buffers: the loads of the next k-block are in flight while the MFMAs of the current
+// one run (the last trip reloads the final k-block instead of reading past the weights).
+template <int RM>
+__device__ __forceinline__ void project_tile(f32x4 (&acc)[RM][kNbPerWave], BFrag& b0,
+                                             const uint16_t* A, int astride,
+                                             const unsigned char* wf, size_t slice, int dkp,
+                                             int lane) {
+#pragma unroll
+  for (int mb = 0; mb < RM; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  BFrag b1;
+  for (int kb = 0; kb < dkp; kb += 2) {
+    load_bfrag(b1, wf, slice, kb + 1);
+    mfma_kblock<RM>(acc, b0, A, astride, kb, lane);
+    load_bfrag(b0, wf, slice, kb + 2 < dkp ? kb + 2 : dkp - 1);
+    mfma_kblock<RM>(acc, b1, A, astride, kb + 1, lane);
+  }
+}
+
+// Gather `rows` embedding rows into the bf16 A tile (row stride astride, dpad columns, zero past
+// d). rid[r] must hold the row's token id, or -1 for a zero row (ids outside [0, V) were already
+// mapped to -1). Eight independent 16-byte loads in flight per thread.
+__device__ __forceinline__ void gather_rows(uint16_t* A, int astride, int rows,
+                                            const int32_t* rid, const uint16_t* E, int d,
+                                            int dpad, int tid, int nthreads) {
+  const int cpr = dpad / 8;  // 16-byte chunks per LDS row
+  for (int i0 = tid; i0 < rows * cpr; i0 += 8 * nthreads) {
+    u32x4 v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = i0 + q * nthreads;
+      v[q] = u32x4{0u, 0u, 0u, 0u};
+      if (i < rows * cpr) {
+        const int r = i / cpr, c = i - r * cpr;
+        const int32_t id = rid[r];
+        if (id >= 0 && c * 8 < d) v[q] = *reinterpret_cast<const u32x4*>(E + (int64_t)id * d + c * 8);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = i0 + q * nthreads;
+      if (i < rows * cpr) {
+        const int r = i / cpr, c = i - r * cpr;
+        *reinterpret_cast<u32x4*>(A + r * astride + c * 8) = v[q];
+      }
+    }
+  }
+}
+
+// Per-wave partial squared norms of the tile's rows: lane l holds rows (l/16)*4 + i of each row
+// block and column l%16 of each column block (padding columns hold zeros); ss[row] receives the
+// sum over this wave's 64 columns.
+template <int RM>
+__device__ __forceinline__ void row_sumsq(const f32x4 (&acc)[RM][kNbPerWave], float* ss,
+                                          int lane) {
+#pragma unroll
+  for (int mb = 0; mb < RM; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < kNbPerWave; ++nb) s = fmaf(acc[mb][nb][i], acc[mb][nb][i], s);
+      s += __shfl_xor(s, 1, kWave);
+      s += __shfl_xor(s, 2, kWave);
+      s += __shfl_xor(s, 4, kWave);
+      s += __shfl_xor(s, 8, kWave);
+      if ((lane & 15) == 0) ss[mb * 16 + (lane >> 4) * 4 + i] = s;
+    }
+  }
+}
+
+}  // namespace lilicorr

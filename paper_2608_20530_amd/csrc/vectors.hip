@@ -19,48 +19,10 @@
 
 #include "common.hpp"
 #include "lilicorr.h"
+#include "projection.hpp"
 
 namespace lilicorr {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kNbPerWave = 4;  // 16-column blocks owned by each wave
-
-struct VecGeom {
-  int d16;    // 16-column blocks of the output
-  int nbp;    // d16 rounded up to whole waves (kNbPerWave blocks each)
-  int dk;     // 32-deep k-blocks of the contraction
-  int dkp;    // dk rounded up to even (the MFMA loop handles two k-blocks per trip)
-  int waves;  // waves per workgroup: one per kNbPerWave column blocks
-  int rm;     // 16-row blocks per workgroup
-};
-
-// rm: up to d = 512, 128-row tiles once there are enough of them to give every compute unit
-// several (a workgroup's phases, gather -> MFMA -> store, then overlap with other workgroups'),
-// else 64-row tiles, which put two workgroups on each compute unit; 32-row tiles above d = 512
-inline VecGeom vec_geom(int d, int64_t M = 0) {
-  VecGeom g;
-  g.d16 = d / 16;
-  g.nbp = (g.d16 + kNbPerWave - 1) / kNbPerWave * kNbPerWave;
-  g.dk = (d + 31) / 32;
-  g.dkp = (g.dk + 1) / 2 * 2;
-  g.waves = g.nbp / kNbPerWave;
-  g.rm = d > 512 ? 2 : ((M + 127) / 128 * 2 >= 2048 ? 8 : 4);
-  return g;
-}
-
-// packed weight layout
-//   [side 2][k-block dkp][term 3][column block nbp][lane 64][8 bf16]: matrix-core B fragments,
-//     lane l of block (kb, nb) holds W[kb*32 + (l/16)*8 + i][nb*16 + l%16], i = 0..7
-//     (0 for rows or columns at or beyond d)
-//   followed by [side 2][d][d] fp32 copies (used by the fp32-embedding kernel)
-inline size_t frag_bytes(int d) {
-  VecGeom g = vec_geom(d);
-  return (size_t)2 * g.dkp * 3 * g.nbp * 1024;
-}
 
 __device__ __forceinline__ uint16_t split_term(float w, int term) {
   float hi = __uint_as_float(__float_as_uint(w) & 0xffff0000u);
@@ -100,40 +62,6 @@ __global__ void pack_weights_kernel(const float* __restrict__ W_in, const float*
   }
 }
 
-typedef u32x4 BFrag[kNbPerWave][3];
-
-// B fragments of k-block kb for the wave's four column blocks, three terms each
-__device__ __forceinline__ void load_bfrag(BFrag& dst, const unsigned char* wf, size_t slice,
-                                           int kb) {
-  const unsigned char* p = wf + (size_t)kb * 3 * slice;
-#pragma unroll
-  for (int t = 0; t < 3; ++t)
-#pragma unroll
-    for (int nb = 0; nb < kNbPerWave; ++nb)
-      dst[nb][t] = *reinterpret_cast<const u32x4*>(p + t * slice + nb * 1024);
-}
-
-// acc[mb][nb] += A[rows of block mb][k-block kb] x B[k-block kb][column block nb], all three
-// terms; the term loop is outermost so consecutive MFMAs never feed each other
-template <int RM>
-__device__ __forceinline__ void mfma_kblock(f32x4 (&acc)[RM][kNbPerWave], const BFrag& b,
-                                            const uint16_t* A, int astride, int kb, int lane) {
-  bf16x8 a[RM];
-  const int kcol = kb * 32 + (lane >> 4) * 8;
-#pragma unroll
-  for (int mb = 0; mb < RM; ++mb)
-    a[mb] = __builtin_bit_cast(
-        bf16x8, *reinterpret_cast<const u32x4*>(A + (mb * 16 + (lane & 15)) * astride + kcol));
-#pragma unroll
-  for (int t = 0; t < 3; ++t)
-#pragma unroll
-    for (int mb = 0; mb < RM; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb)
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            a[mb], __builtin_bit_cast(bf16x8, b[nb][t]), acc[mb][nb], 0, 0, 0);
-}
-
 // One workgroup: RM*16 candidate rows x all d columns of one side. The gathered embedding rows
 // (the A operand) are staged once in LDS; wave w owns column blocks [4w, 4w+4). Each B fragment
 // feeds RM MFMAs and each A fragment 12.
@@ -162,73 +90,22 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   const size_t slice = (size_t)nbp * 1024;
   const unsigned char* wf =
       frags + (size_t)side * dkp * 3 * slice + (size_t)wave * kNbPerWave * 1024 + lane * 16;
-  BFrag b0, b1;
+  BFrag b0;
   load_bfrag(b0, wf, slice, 0);  // in flight during the gather
 
-  // gather the embedding rows (zero rows past M or for ids outside [0, V); zero k-padding):
-  // the ids first, then eight independent 16-byte row loads in flight per thread
+  // gather the embedding rows (zero rows past M or for ids outside [0, V); zero k-padding)
   for (int r = tid; r < ROWS; r += nthreads) {
     const int64_t row = row0 + r;
     const int32_t id = row < M ? ids[row] : -1;
     rid[r] = (id >= 0 && id < V) ? id : -1;
   }
   __syncthreads();
-  const int cpr = dpad / 8;  // 16-byte chunks per LDS row
-  for (int i0 = tid; i0 < ROWS * cpr; i0 += 8 * nthreads) {
-    u32x4 v[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int i = i0 + q * nthreads;
-      v[q] = u32x4{0u, 0u, 0u, 0u};
-      if (i < ROWS * cpr) {
-        const int r = i / cpr, c = i - r * cpr;
-        const int32_t id = rid[r];
-        if (id >= 0 && c * 8 < d) v[q] = *reinterpret_cast<const u32x4*>(E + (int64_t)id * d + c * 8);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int i = i0 + q * nthreads;
-      if (i < ROWS * cpr) {
-        const int r = i / cpr, c = i - r * cpr;
-        *reinterpret_cast<u32x4*>(A + r * astride + c * 8) = v[q];
-      }
-    }
-  }
+  gather_rows(A, astride, ROWS, rid, E, d, dpad, tid, nthreads);
   __syncthreads();
 
   f32x4 acc[RM][kNbPerWave];
-#pragma unroll
-  for (int mb = 0; mb < RM; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // two k-blocks per trip through two register buffers: the loads of the next k-block are in
-  // flight while the MFMAs of the current one run (the last trip reloads the final k-block
-  // instead of reading past the packed weights)
-  for (int kb = 0; kb < dkp; kb += 2) {
-    load_bfrag(b1, wf, slice, kb + 1);
-    mfma_kblock<RM>(acc, b0, A, astride, kb, lane);
-    load_bfrag(b0, wf, slice, kb + 2 < dkp ? kb + 2 : dkp - 1);
-    mfma_kblock<RM>(acc, b1, A, astride, kb + 1, lane);
-  }
-
-  // row norms: lane l holds rows (l/16)*4 + i of each row block, column l%16 of each column block
-  // (padding columns hold zeros)
-#pragma unroll
-  for (int mb = 0; mb < RM; ++mb) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float ss = 0.f;
-#pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb) ss = fmaf(acc[mb][nb][i], acc[mb][nb][i], ss);
-      ss += __shfl_xor(ss, 1, kWave);
-      ss += __shfl_xor(ss, 2, kWave);
-      ss += __shfl_xor(ss, 4, kWave);
-      ss += __shfl_xor(ss, 8, kWave);
-      if ((lane & 15) == 0) ssbuf[wave * ROWS + mb * 16 + (lane >> 4) * 4 + i] = ss;
-    }
-  }
+  project_tile<RM>(acc, b0, A, astride, wf, slice, dkp, lane);
+  row_sumsq<RM>(acc, ssbuf + wave * ROWS, lane);
   __syncthreads();
   float* out = side == 0 ? in_vec : out_vec;
   const int col0 = wave * kNbPerWave * 16 + (lane & 15);
@@ -322,7 +199,7 @@ using namespace lilicorr;
 
 extern "C" size_t lilicorr_packed_weight_bytes(int d) {
   if (!vec_d_ok(d)) return 0;
-  return frag_bytes(d) + (size_t)2 * d * d * sizeof(float);
+  return packed_bytes(d);
 }
 
 extern "C" lilicorr_status lilicorr_pack_weights(const float* W_in, const float* W_out, int d,

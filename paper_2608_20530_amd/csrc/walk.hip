@@ -22,24 +22,6 @@ constexpr int kWalkThreads = 256;
 constexpr int kSegRows = 2048;  // table rows per segment (slots per segment: kSegRows / K)
 constexpr int kRowBatch = 16;   // rows per group whose loads are issued together
 
-// all-reduce over aligned groups of G lanes; every lane of a group receives the group's result
-template <typename Op>
-__device__ __forceinline__ float dpp_allreduce16(float v, Op op) {
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false)));   // quad_perm 1,0,3,2
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xf, 0xf, false)));   // quad_perm 2,3,0,1
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xf, 0xf, false)));  // row_half_mirror
-  v = op(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xf, 0xf, false)));  // row_mirror
-  return v;
-}
-
-template <int G, typename Op>
-__device__ __forceinline__ float group_allreduce(float v, Op op) {
-  v = dpp_allreduce16(v, op);
-  if (G >= 32) v = op(v, __shfl_xor(v, 16, kWave));
-  if (G >= 64) v = op(v, __shfl_xor(v, 32, kWave));
-  return v;
-}
-
 template <int G>
 __global__ __launch_bounds__(kWalkThreads) void greedy_walk_kernel(
     const float* __restrict__ S, const float* __restrict__ S0, const float* __restrict__ logp,
@@ -52,12 +34,9 @@ __global__ __launch_bounds__(kWalkThreads) void greedy_walk_kernel(
 
   const int64_t n = blockIdx.x;
   const int tid = threadIdx.x;
-  const int lane = lane_id();
   const int j = tid % G;                 // candidate index within the row
   const int group = tid / G;
   constexpr int kGroups = kWalkThreads / G;
-  const int gshift = (lane / G) * G;     // first ballot bit of this lane's group
-  const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
   const bool live = j < K;
   const bool use_lp = lambda != 0.f;
   const float* Sn = S ? S + n * (B - 1) * (int64_t)K * K : nullptr;
@@ -92,13 +71,10 @@ __global__ __launch_bounds__(kWalkThreads) void greedy_walk_kernel(
 #pragma unroll
       for (int u = 0; u < kRowBatch; ++u) {
         const int64_t row = base + group + (int64_t)u * kGroups;
-        const float m = group_allreduce<G>(z[u], [](float a, float b) { return fmaxf(a, b); });
-        const uint64_t hits = (__ballot(live && z[u] == m) >> gshift) & gmask;
-        const int arg = hits ? __ffsll((long long)hits) - 1 : 0;  // no hit only with NaN scores
-        const float s = group_allreduce<G>(live ? expf(z[u] - m) : 0.f,
-                                           [](float a, float b) { return a + b; });
-        if (j == 0 && row < re)
-          table[row - rb] = (uint64_t)(uint32_t)arg | ((uint64_t)__float_as_uint(-logf(s)) << 32);
+        int arg;
+        float lq;
+        resolve_row<G>(z[u], live, arg, lq);
+        if (j == 0 && row < re) table[row - rb] = table_entry(arg, lq);
       }
     }
     __syncthreads();

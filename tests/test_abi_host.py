@@ -27,7 +27,8 @@ def test_header_declares_the_path(L):
     names = _declared()
     for n in ["lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_pack_weights",
               "lilicorr_packed_weight_bytes", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
-              "lilicorr_greedy_walk", "lilicorr_status_string"]:
+              "lilicorr_greedy_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+              "lilicorr_status_string"]:
         assert n in names
 
 
@@ -114,6 +115,39 @@ def test_other_argument_errors(L):
     assert lib.lilicorr_greedy_walk(*bad) == -2
     bad = list(gw); bad[8] = A + 4
     assert lib.lilicorr_greedy_walk(*bad) == -3
+
+
+def test_score_walk_sizes_and_argument_errors(L):
+    lib = L.load_library()
+    # 256-byte block of per-request counters, then N x (1 + (B-1) K) 8-byte table rows
+    assert L.lilicorr_score_walk_workspace_bytes(64, 16, 16) == 256 + 64 * 241 * 8
+    assert L.lilicorr_score_walk_workspace_bytes(2, 3, 4) == 256 + 2 * 9 * 8
+    assert L.lilicorr_score_walk_workspace_bytes(65, 1, 1) == 512 + 65 * 8
+    assert L.lilicorr_score_walk_workspace_bytes(1, 2, 65) == 0
+    assert L.lilicorr_score_walk_workspace_bytes(1, 20000, 1) == 0
+    ws = L.lilicorr_score_walk_workspace_bytes(2, 3, 4)
+    ok = [A, A, A, 1, 1000, 64, A, None, 2, 3, 4, 8.0, 0.0, None, None, A, None, None, A, ws, None]
+    def call(**kw):
+        names = ["ids", "logp", "E", "e_dtype", "V", "d", "packed", "anchor", "N", "B", "K",
+                 "sigma", "lw", "S", "S0", "draft", "choice", "logq", "ws", "ws_bytes", "stream"]
+        args = list(ok)
+        for k, v in kw.items():
+            args[names.index(k)] = v
+        return lib.lilicorr_score_walk(*args)
+    assert call(ids=None) == -1
+    assert call(draft=None) == -1
+    assert call(ws=None) == -1
+    assert call(e_dtype=7) == -1
+    assert call(sigma=float("nan")) == -1
+    assert call(lw=float("inf")) == -1
+    assert call(e_dtype=0) == -2        # fp32 embeddings: use the separate calls
+    assert call(d=512) == -2            # above the fused path's d
+    assert call(d=40) == -2
+    assert call(K=65) == -2
+    assert call(B=20000, K=1) == -2     # the request's table would not fit in LDS
+    assert call(draft=A + 4) == -3
+    assert call(anchor=A + 8) == -3
+    assert call(ws_bytes=ws - 1) == -4
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
