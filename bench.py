@@ -67,7 +67,7 @@ def traffic_per_launch():
 
 
 def time_logits_pass(L, torch, cfg, logits_list, iters, warmup):
-    """Average duration (s) of the logits-pass kernel over `iters` cold launches."""
+    """Durations (s) of the logits-pass kernel over `iters` cold launches: mean, median, p10, p90."""
     K = cfg.K
     N, B, V = logits_list[0].shape
     ids = torch.empty(N, B, K, dtype=torch.int32, device="cuda")
@@ -84,7 +84,45 @@ def time_logits_pass(L, torch, cfg, logits_list, iters, warmup):
         L.topk(logits_list[i % len(logits_list)], K, out=(ids, logp), workspace=ws)
         ev[i][1].record()
     torch.cuda.synchronize()
-    return statistics.mean(a.elapsed_time(b) for a, b in ev) / 1e3
+    t = sorted(a.elapsed_time(b) / 1e3 for a, b in ev)
+    q = lambda f: t[min(len(t) - 1, int(f * len(t)))]
+    return statistics.mean(t), statistics.median(t), q(0.1), q(0.9)
+
+
+def stream_read_rate(torch, bufs, iters=20, warmup=3):
+    """GB/s of a plain streaming read (16-byte streaming-policy buffer loads, the logits pass's own
+    load path, one contiguous segment per workgroup) over the same resident buffers, rotated like
+    the logits pass reads them: the read ceiling the logits pass is compared with."""
+    import ctypes
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_20530_amd", "libbench_read.so"))
+    lib.bench_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                      ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_read.restype = ctypes.c_int
+    grid = 1024
+    sink = torch.empty(grid * 256, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def run(i):
+        b = bufs[i % len(bufs)]
+        rc = lib.bench_stream_read(b.data_ptr(), b.numel() * b.element_size(), sink.data_ptr(),
+                                   grid, stream)
+        if rc != 0:
+            raise RuntimeError(f"bench_stream_read failed ({rc})")
+
+    for i in range(warmup):
+        run(i)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+    torch.cuda.synchronize()
+    for i in range(iters):
+        ev[i][0].record()
+        run(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    sec = statistics.mean(a.elapsed_time(b) for a, b in ev) / 1e3
+    nbytes = bufs[0].numel() * bufs[0].element_size()
+    return nbytes / sec / 1e9
 
 
 def cpu_baseline(cfg, inp, seconds):
@@ -232,16 +270,22 @@ def main():
         lg4 = workloads.make_logits(c4).cuda()
         print(f"[bench] stress logits generated in {time.perf_counter() - t:.1f} s", file=sys.stderr,
               flush=True)
-        t3 = time_logits_pass(L, torch, cfg, logits_list, iters=50, warmup=5)
+        t3, m3, lo3, hi3 = time_logits_pass(L, torch, cfg, logits_list, iters=50, warmup=5)
+        read3 = stream_read_rate(torch, logits_list)
         del logits_list
         torch.cuda.empty_cache()
-        t4 = time_logits_pass(L, torch, c4, [lg4], iters=20, warmup=3)
+        t4, m4, lo4, hi4 = time_logits_pass(L, torch, c4, [lg4], iters=20, warmup=3)
+        read4 = stream_read_rate(torch, [lg4])
         b4 = c4.N * c4.B * c4.V * 2 + c4.N * c4.B * c4.K * 8
         out["logits_pass"] = {
             "headline": {"GB_s": algo_bytes / t3 / 1e9, "us": t3 * 1e6,
-                         "frac_of_8TBs": algo_bytes / t3 / 1e9 / PEAK_HBM_GBS},
+                         "us_median": m3 * 1e6, "us_p10": lo3 * 1e6, "us_p90": hi3 * 1e6,
+                         "frac_of_8TBs": algo_bytes / t3 / 1e9 / PEAK_HBM_GBS,
+                         "stream_read_GB_s": read3},
             "stress": {"GB_s": b4 / t4 / 1e9, "us": t4 * 1e6,
+                       "us_median": m4 * 1e6, "us_p10": lo4 * 1e6, "us_p90": hi4 * 1e6,
                        "frac_of_8TBs": b4 / t4 / 1e9 / PEAK_HBM_GBS,
+                       "stream_read_GB_s": read4,
                        "workload": "N=256, B=16, K=32, V=262144, bf16 logits"},
         }
         del lg4
