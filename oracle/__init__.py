@@ -45,8 +45,9 @@ def _load():
         lib.oracle_candidate_vectors.argtypes = [P, P, I, I64, I, P, P, I64, I64, I, P, P]
         lib.oracle_pair_scores.argtypes = [P, P, P, I64, I64, I, I, ctypes.c_float, P, P]
         lib.oracle_greedy_walk.argtypes = [P, P, P, P, I64, I64, I, ctypes.c_float, P, P, P]
+        lib.oracle_viterbi_walk.argtypes = [P, P, P, P, I64, I64, I, ctypes.c_float, P, P, P, P]
         for f in (lib.oracle_topk, lib.oracle_candidate_vectors, lib.oracle_pair_scores,
-                  lib.oracle_greedy_walk):
+                  lib.oracle_greedy_walk, lib.oracle_viterbi_walk):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -126,3 +127,22 @@ def greedy_walk(S: np.ndarray, S0, logp: np.ndarray, ids: np.ndarray, logp_weigh
                                       float(logp_weight), _ptr(draft), _ptr(choice), _ptr(logq)),
            "greedy_walk")
     return draft, choice, logq
+
+
+def viterbi_walk(S: np.ndarray, S0, logp: np.ndarray, ids: np.ndarray, logp_weight: float = 0.0):
+    """Exact max-path decode -> draft [N, B] int32, choice [N, B] int32, logq [N, B] f32,
+    score [N] f32 (the path score g)."""
+    logp = np.ascontiguousarray(logp, dtype=np.float32)
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    N, B, K = ids.shape
+    S = np.ascontiguousarray(S, dtype=np.float32)
+    if S0 is not None:
+        S0 = np.ascontiguousarray(S0, dtype=np.float32)
+    draft = np.zeros((N, B), np.int32)
+    choice = np.zeros((N, B), np.int32)
+    logq = np.zeros((N, B), np.float32)
+    score = np.zeros((N,), np.float32)
+    _check(_load().oracle_viterbi_walk(_ptr(S), _ptr(S0), _ptr(logp), _ptr(ids), N, B, K,
+                                       float(logp_weight), _ptr(draft), _ptr(choice), _ptr(logq),
+                                       _ptr(score)), "viterbi_walk")
+    return draft, choice, logq, score

@@ -261,3 +261,100 @@ int oracle_greedy_walk(const float *S, const float *S0, const float *logp, const
     free(z);
     return 0;
 }
+
+/* ---------------------------------------------------------------------------------------------
+ * Exact max-path decode (decode-rule appendix, Eq. pathscore): the path c = (c_0 .. c_{B-1})
+ * that maximises the sum of its matching terms
+ *     g(c) = P_0[c_0] + sum_{t=1}^{B-1} phi(t-1, c_{t-1}, c_t)   (+ lambda sum_t logp[t][c_t])
+ * with P_0 = S0, or all zero without an anchor (slot 0's candidate is then free). Sweeping left
+ * to right, best[k] is the score of the best path ending at candidate k of the current slot and
+ * from[t][k] the predecessor it came through; the path is then traced back from the best
+ * candidate of the last slot. Ties go to the lowest index, for predecessors and for the final
+ * candidate: among all maximising paths this returns the one that is smallest when read from the
+ * last slot backwards.
+ * The sums and comparisons run in float, one rounding per addition (and one fmaf for the lambda
+ * term): the precision the GPU kernel decides in, so both sides take the same decisions.
+ * logq[t] is Eq. (localar) along the returned path, z_t[k] = P_t(c_{t-1}, k) (+ lambda logp),
+ * logq[t] = z_t[c_t] - log sum_k exp z_t[k], in double from the float z; score[n] = g (float).
+ * ------------------------------------------------------------------------------------------- */
+
+int oracle_viterbi_walk(const float *S, const float *S0, const float *logp, const int32_t *ids,
+                        int64_t N, int64_t B, int K, float logp_weight, int32_t *draft,
+                        int32_t *choice, float *logq, float *score)
+{
+    if (!logp || !ids || !draft || N < 0 || B < 1 || K < 1)
+        return -1;
+    if (B > 1 && !S)
+        return -1;
+    float *best = (float *)malloc(sizeof(float) * (size_t)K);
+    float *next = (float *)malloc(sizeof(float) * (size_t)K);
+    float *z = (float *)malloc(sizeof(float) * (size_t)K);
+    int *from = (int *)malloc(sizeof(int) * (size_t)(B * K));
+    int *path = (int *)malloc(sizeof(int) * (size_t)B);
+    for (int64_t n = 0; n < N; ++n) {
+        for (int k = 0; k < K; ++k) {
+            float v = S0 ? S0[n * K + k] : 0.0f;
+            if (logp_weight != 0.0f)
+                v = fmaf(logp_weight, logp[(n * B + 0) * K + k], v);
+            best[k] = v;
+        }
+        for (int64_t t = 1; t < B; ++t) {
+            const float *St = S + (n * (B - 1) + (t - 1)) * K * (int64_t)K;
+            for (int k = 0; k < K; ++k) {
+                float bv = best[0] + St[0 * K + k];
+                int bp = 0;
+                for (int p = 1; p < K; ++p) {
+                    const float v = best[p] + St[p * K + k];
+                    if (v > bv) {
+                        bv = v;
+                        bp = p;
+                    }
+                }
+                if (logp_weight != 0.0f)
+                    bv = fmaf(logp_weight, logp[(n * B + t) * K + k], bv);
+                next[k] = bv;
+                from[t * K + k] = bp;
+            }
+            memcpy(best, next, sizeof(float) * (size_t)K);
+        }
+        int c = 0;
+        for (int k = 1; k < K; ++k)
+            if (best[k] > best[c])
+                c = k;
+        if (score)
+            score[n] = best[c];
+        path[B - 1] = c;
+        for (int64_t t = B - 1; t >= 1; --t)
+            path[t - 1] = from[t * K + path[t]];
+        for (int64_t t = 0; t < B; ++t) {
+            for (int k = 0; k < K; ++k) {
+                float pair;
+                if (t == 0)
+                    pair = S0 ? S0[n * K + k] : 0.0f;
+                else
+                    pair = S[((n * (B - 1) + (t - 1)) * K + path[t - 1]) * K + k];
+                z[k] = (logp_weight == 0.0f) ? pair
+                                              : fmaf(logp_weight, logp[(n * B + t) * K + k], pair);
+            }
+            double m = -INFINITY;
+            for (int k = 0; k < K; ++k)
+                if ((double)z[k] > m)
+                    m = (double)z[k];
+            double s = 0.0;
+            for (int k = 0; k < K; ++k)
+                s += exp((double)z[k] - m);
+            const int ct = path[t];
+            draft[n * B + t] = ids[(n * B + t) * K + ct];
+            if (choice)
+                choice[n * B + t] = ct;
+            if (logq)
+                logq[n * B + t] = (float)((double)z[ct] - (m + log(s)));
+        }
+    }
+    free(best);
+    free(next);
+    free(z);
+    free(from);
+    free(path);
+    return 0;
+}
