@@ -132,6 +132,25 @@ lilicorr_status lilicorr_greedy_walk(const float *S, const float *S0, const floa
                                      float *logq, hipStream_t stream);
 
 /*
+ * Exact max-path decode (the decode-rule appendix): the path c = (c_0 .. c_{B-1}) maximising
+ * Eq. (pathscore), g(c) = P_0[c_0] + sum_{t>=1} S[n][t-1][c_{t-1}][c_t]
+ * (+ logp_weight * sum_t logp[n][t][c_t]), with P_0 = S0[n] or all zero when S0 is NULL, found
+ * by dynamic programming in O(B K^2). Ties go to the lowest index (predecessor and final
+ * candidate), which returns, among all maximising paths, the smallest read from the last slot
+ * backwards. Sums and comparisons are fp32 with one rounding per addition.
+ *   S, S0, logp, ids, logp_weight   as for lilicorr_greedy_walk.
+ *   draft, choice  [N][B] int32 out (choice may be NULL): the path's tokens and indices.
+ *   logq           [N][B] fp32 out or NULL: Eq. (localar) along the path,
+ *                  z_t[c_t] - log sum_k exp z_t[k] with z_t[k] = P_t(c_{t-1}, k) (+ lambda logp).
+ *   score          [N] fp32 out or NULL: g of the returned path.
+ * Limits: K <= 64, B <= 8192, B * K <= 65536 (LILICORR_ERR_UNSUPPORTED otherwise).
+ */
+lilicorr_status lilicorr_viterbi_walk(const float *S, const float *S0, const float *logp,
+                                      const int32_t *ids, int64_t N, int64_t B, int K,
+                                      float logp_weight, int32_t *draft, int32_t *choice,
+                                      float *logq, float *score, hipStream_t stream);
+
+/*
  * Steps 2-4 in one pass (Sec. 3.5: all pair matrices in one batched pass, then the greedy walk;
  * the implementation appendix serves matching and selection as a single replay): the draft,
  * choice and logq that lilicorr_candidate_vectors -> lilicorr_pair_scores -> lilicorr_greedy_walk

@@ -7,6 +7,7 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
   lilicorr_candidate_vectors  ids, E -> in_vec, out_vec [N,B,K,d]       (Sec. 3.2 unit-norm heads)
   lilicorr_pair_scores        in/out -> S [N,B-1,K,K] (+ S0 [N,K])      (Eq. pair)
   lilicorr_greedy_walk        S, S0, logp, ids -> draft, choice, logq   (Sec. 3.5, Eq. localar)
+  lilicorr_viterbi_walk       S, S0, logp, ids -> best path, logq, g    (Eq. pathscore)
   lilicorr_score_walk         ids, logp, E -> draft, choice, logq       (steps 2-4 in one pass)
 
 This module only marshals arguments: torch supplies device memory and the current HIP stream,
@@ -24,9 +25,9 @@ __all__ = [
     "LIB_PATH", "load_library", "LilicorrError", "SIGMA",
     "lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
-    "lilicorr_greedy_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+    "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
     "lilicorr_status_string",
-    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "score_walk",
+    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk",
     "draft_block",
 ]
 
@@ -60,6 +61,7 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_candidate_vectors": ([P, P, I, I64, I, P, I64, I64, I, P, P, P], I),
         "lilicorr_pair_scores": ([P, P, P, I64, I64, I, I, F, P, P, P], I),
         "lilicorr_greedy_walk": ([P, P, P, P, I64, I64, I, F, P, P, P, P], I),
+        "lilicorr_viterbi_walk": ([P, P, P, P, I64, I64, I, F, P, P, P, P, P], I),
         "lilicorr_score_walk_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_walk": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, SZ,
                                  P], I),
@@ -116,6 +118,12 @@ def lilicorr_pair_scores(in_vec, out_vec, anchor_out, N, B, K, d, sigma, S, S0, 
 def lilicorr_greedy_walk(S, S0, logp, ids, N, B, K, logp_weight, draft, choice, logq, stream):
     return _call("lilicorr_greedy_walk", S, S0, logp, ids, N, B, K, logp_weight, draft, choice,
                  logq, stream)
+
+
+def lilicorr_viterbi_walk(S, S0, logp, ids, N, B, K, logp_weight, draft, choice, logq, score,
+                          stream):
+    return _call("lilicorr_viterbi_walk", S, S0, logp, ids, N, B, K, logp_weight, draft, choice,
+                 logq, score, stream)
 
 
 def lilicorr_score_walk_workspace_bytes(N: int, B: int, K: int) -> int:
@@ -226,6 +234,27 @@ def greedy_walk(S: torch.Tensor, S0, logp: torch.Tensor, ids: torch.Tensor,
                          _dev(draft, "draft", (torch.int32,)), _dev(choice, "choice", (torch.int32,)),
                          _dev(logq, "logq", (torch.float32,)), _stream())
     return draft, choice, logq
+
+
+def viterbi_walk(S: torch.Tensor, S0, logp: torch.Tensor, ids: torch.Tensor,
+                 logp_weight: float = 0.0, *, out=None):
+    """Exact max-path decode -> (draft [N,B] int32, choice [N,B] int32, logq [N,B] fp32,
+    score [N] fp32)."""
+    N, B, K = ids.shape
+    if out is None:
+        out = (torch.empty(N, B, dtype=torch.int32, device=ids.device),
+               torch.empty(N, B, dtype=torch.int32, device=ids.device),
+               torch.empty(N, B, dtype=torch.float32, device=ids.device),
+               torch.empty(N, dtype=torch.float32, device=ids.device))
+    draft, choice, logq, score = out
+    lilicorr_viterbi_walk(_dev(S, "S", (torch.float32,)) if B > 1 else None,
+                          _dev(S0, "S0", (torch.float32,)), _dev(logp, "logp", (torch.float32,)),
+                          _dev(ids, "ids", (torch.int32,)), N, B, K, float(logp_weight),
+                          _dev(draft, "draft", (torch.int32,)),
+                          _dev(choice, "choice", (torch.int32,)),
+                          _dev(logq, "logq", (torch.float32,)),
+                          _dev(score, "score", (torch.float32,)), _stream())
+    return draft, choice, logq, score
 
 
 def score_walk_workspace(N: int, B: int, K: int, device="cuda") -> torch.Tensor:

@@ -27,7 +27,7 @@ def test_header_declares_the_path(L):
     names = _declared()
     for n in ["lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_pack_weights",
               "lilicorr_packed_weight_bytes", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
-              "lilicorr_greedy_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+              "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
               "lilicorr_status_string"]:
         assert n in names
 
@@ -115,6 +115,25 @@ def test_other_argument_errors(L):
     assert lib.lilicorr_greedy_walk(*bad) == -2
     bad = list(gw); bad[8] = A + 4
     assert lib.lilicorr_greedy_walk(*bad) == -3
+
+
+def test_viterbi_argument_errors(L):
+    lib = L.load_library()
+    vw = [A, None, A, A, 2, 3, 4, 0.0, A, None, None, None, None]
+    bad = list(vw); bad[0] = None
+    assert lib.lilicorr_viterbi_walk(*bad) == -1      # S required when B > 1
+    bad = list(vw); bad[8] = None
+    assert lib.lilicorr_viterbi_walk(*bad) == -1      # draft
+    bad = list(vw); bad[7] = float("nan")
+    assert lib.lilicorr_viterbi_walk(*bad) == -1
+    bad = list(vw); bad[6] = 65
+    assert lib.lilicorr_viterbi_walk(*bad) == -2      # K > 64
+    bad = list(vw); bad[5] = 8193
+    assert lib.lilicorr_viterbi_walk(*bad) == -2      # B > 8192
+    bad = list(vw); bad[5], bad[6] = 2000, 64
+    assert lib.lilicorr_viterbi_walk(*bad) == -2      # B * K > 65536
+    bad = list(vw); bad[11] = A + 4
+    assert lib.lilicorr_viterbi_walk(*bad) == -3      # score alignment
 
 
 def test_score_walk_sizes_and_argument_errors(L):
