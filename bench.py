@@ -125,6 +125,21 @@ def stream_read_rate(torch, bufs, iters=20, warmup=3):
     return nbytes / sec / 1e9
 
 
+def median_launch_us(torch, fn, iters=50, warmup=5):
+    """Median duration of one call of fn, from HIP events on the current stream."""
+    for _ in range(warmup):
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in ev) * 1e3
+
+
 def cpu_baseline(cfg, inp, seconds):
     """The oracle chain, single-threaded, on whole requests of the workload until `seconds`."""
     import numpy as np
@@ -262,6 +277,28 @@ def main():
         "separate_calls": {"path": "topk -> candidate_vectors -> pair_scores -> greedy_walk",
                            "ms_per_step": sep_elapsed / args.steps * 1e3,
                            "value": N * args.steps / sep_elapsed},
+    }
+
+    # the two decode rules of the decode-rule appendix, each in the fused pass and stand-alone,
+    # on the candidates of the last timed step
+    ws_exact = L.score_viterbi_workspace(N, B, K)
+    score = torch.empty(N, dtype=torch.float32, device=dev)
+    L.pair_scores(*L.candidate_vectors(ids, E, packed, out=(in_vec, out_vec)), None, L.SIGMA,
+                  out=(S, None))
+    fused_greedy = median_launch_us(torch, lambda: L.score_walk(
+        ids, logp, E, packed, out=(draft, choice, logq), workspace=ws_fused))
+    fused_exact = median_launch_us(torch, lambda: L.score_viterbi(
+        ids, logp, E, packed, out=(draft, choice, logq, score), workspace=ws_exact))
+    out["decode_rules"] = {
+        "fused_greedy_us": fused_greedy,
+        "fused_exact_us": fused_exact,
+        "greedy_walk_us": median_launch_us(torch, lambda: L.greedy_walk(
+            S, None, logp, ids, 0.0, out=(draft, choice, logq))),
+        "viterbi_walk_us": median_launch_us(torch, lambda: L.viterbi_walk(
+            S, None, logp, ids, 0.0, out=(draft, choice, logq, score))),
+        "step_us_greedy": topk_s * 1e6 + fused_greedy,
+        "step_us_exact": topk_s * 1e6 + fused_exact,
+        "note": "median call durations (HIP events); steps add the mean logits-pass launch",
     }
 
     if not args.no_stress:

@@ -178,6 +178,24 @@ lilicorr_status lilicorr_score_walk(const int32_t *ids, const float *logp, const
                                     float *S0, int32_t *draft, int32_t *choice, float *logq,
                                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * The same single pass with the exact max-path decode in place of the greedy walk (the decode-rule
+ * appendix serves each rule as one fused kernel): the draft, choice, logq and score that
+ * lilicorr_candidate_vectors -> lilicorr_pair_scores -> lilicorr_viterbi_walk give on the same
+ * inputs. Arguments as for lilicorr_score_walk, plus score ([N] fp32 or NULL, as for
+ * lilicorr_viterbi_walk); workspace of lilicorr_score_viterbi_workspace_bytes(N, B, K) bytes,
+ * zero-filled once, with the same rules. Limits: K <= 64, B <= 8192, B * K <= 65536, bf16 E,
+ * d a multiple of 16 and at most 256.
+ */
+size_t lilicorr_score_viterbi_workspace_bytes(int64_t N, int64_t B, int K);
+lilicorr_status lilicorr_score_viterbi(const int32_t *ids, const float *logp, const void *E,
+                                       lilicorr_dtype e_dtype, int64_t V, int d,
+                                       const void *packed_w, const float *anchor_out, int64_t N,
+                                       int64_t B, int K, float sigma, float logp_weight, float *S,
+                                       float *S0, int32_t *draft, int32_t *choice, float *logq,
+                                       float *score, void *workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char *lilicorr_status_string(lilicorr_status s);
 

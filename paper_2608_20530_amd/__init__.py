@@ -9,6 +9,7 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
   lilicorr_greedy_walk        S, S0, logp, ids -> draft, choice, logq   (Sec. 3.5, Eq. localar)
   lilicorr_viterbi_walk       S, S0, logp, ids -> best path, logq, g    (Eq. pathscore)
   lilicorr_score_walk         ids, logp, E -> draft, choice, logq       (steps 2-4 in one pass)
+  lilicorr_score_viterbi      the same pass with the exact max-path decode
 
 This module only marshals arguments: torch supplies device memory and the current HIP stream,
 and every step of the path runs in the library's kernels. There is no fallback: if the library
@@ -26,8 +27,9 @@ __all__ = [
     "lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
     "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+    "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes",
     "lilicorr_status_string",
-    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk",
+    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk", "score_viterbi",
     "draft_block",
 ]
 
@@ -65,6 +67,9 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_score_walk_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_walk": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, SZ,
                                  P], I),
+        "lilicorr_score_viterbi_workspace_bytes": ([I64, I64, I], SZ),
+        "lilicorr_score_viterbi": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, P,
+                                    SZ, P], I),
         "lilicorr_status_string": ([I], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -135,6 +140,18 @@ def lilicorr_score_walk(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
     return _call("lilicorr_score_walk", ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
                  K, sigma, logp_weight, S, S0, draft, choice, logq, workspace, workspace_bytes,
                  stream)
+
+
+def lilicorr_score_viterbi_workspace_bytes(N: int, B: int, K: int) -> int:
+    return int(load_library().lilicorr_score_viterbi_workspace_bytes(N, B, K))
+
+
+def lilicorr_score_viterbi(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K, sigma,
+                           logp_weight, S, S0, draft, choice, logq, score, workspace,
+                           workspace_bytes, stream):
+    return _call("lilicorr_score_viterbi", ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N,
+                 B, K, sigma, logp_weight, S, S0, draft, choice, logq, score, workspace,
+                 workspace_bytes, stream)
 
 
 # ---- torch conveniences (marshalling only) -----------------------------------------------------
@@ -294,6 +311,49 @@ def score_walk(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor, packed: t
     if scores:
         return draft, choice, logq, S, S0
     return draft, choice, logq
+
+
+def score_viterbi_workspace(N: int, B: int, K: int, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace for score_viterbi (the library keeps it zeroed between calls)."""
+    need = lilicorr_score_viterbi_workspace_bytes(N, B, K)
+    if need == 0:
+        raise LilicorrError(f"score_viterbi does not support N={N}, B={B}, K={K}")
+    return torch.zeros(need, dtype=torch.uint8, device=device)
+
+
+def score_viterbi(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor, packed: torch.Tensor,
+                  anchor_out=None, sigma: float = SIGMA, logp_weight: float = 0.0, *,
+                  scores: bool = False, out=None, workspace=None):
+    """Steps 2-4 with the exact decode -> (draft, choice, logq, score[, S, S0 when scores=True])."""
+    N, B, K = ids.shape
+    V, d = E.shape
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.float32, device=dev),
+               torch.empty(N, dtype=torch.float32, device=dev))
+    draft, choice, logq, score = out
+    S = S0 = None
+    if scores:
+        S = torch.empty(N, max(B - 1, 0), K, K, dtype=torch.float32, device=dev)
+        S0 = torch.empty(N, K, dtype=torch.float32, device=dev) if anchor_out is not None else None
+    if workspace is None:
+        workspace = score_viterbi_workspace(N, B, K, dev)
+    lilicorr_score_viterbi(_dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)),
+                           _dev(E, "E", (torch.bfloat16, torch.float32)), _dtype_code(E), V, d,
+                           _dev(packed, "packed"),
+                           _dev(anchor_out, "anchor_out", (torch.float32,)), N, B, K,
+                           float(sigma), float(logp_weight),
+                           _dev(S, "S", (torch.float32,)) if S is not None and B > 1 else None,
+                           _dev(S0, "S0", (torch.float32,)), _dev(draft, "draft", (torch.int32,)),
+                           _dev(choice, "choice", (torch.int32,)),
+                           _dev(logq, "logq", (torch.float32,)),
+                           _dev(score, "score", (torch.float32,)), _dev(workspace, "workspace"),
+                           workspace.numel(), _stream())
+    if scores:
+        return draft, choice, logq, score, S, S0
+    return draft, choice, logq, score
 
 
 def draft_block(logits: torch.Tensor, K: int, E: torch.Tensor, packed: torch.Tensor,

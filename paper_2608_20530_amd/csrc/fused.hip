@@ -17,6 +17,9 @@
 //  6. the workgroup takes a ticket; the last one of its request to finish stages the request's
 //     table in LDS, follows it slot by slot and writes draft, choice and logq.
 // The anchor pair (when given) has a workgroup of its own: in rows of slot 0 against anchor_out.
+// The exact max-path variant (decode-rule appendix) replaces steps 5-6: every workgroup writes its
+// score blocks to the workspace and the request's last workgroup runs the dynamic program over
+// all of them (viterbi_block), as the paper serves both decode rules as one fused kernel each.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -24,6 +27,7 @@
 #include "common.hpp"
 #include "lilicorr.h"
 #include "projection.hpp"
+#include "viterbi.hpp"
 
 namespace lilicorr {
 namespace {
@@ -32,6 +36,9 @@ constexpr int kSideRows = 64;                // candidate rows per side per work
 constexpr int kSideRm = kSideRows / 16;      // 16-row blocks per side
 constexpr int kFusedMaxD = 256;              // the fp32 projections of both sides fit in LDS
 constexpr int64_t kMaxTableRows = 16384;     // a request's table is staged in LDS at the end
+constexpr int64_t kMaxExactSlots = 8192;     // exact decode: B bytes of path in LDS
+constexpr int64_t kMaxExactBackPointers = 65536;  // exact decode: B * K bytes of predecessors
+constexpr size_t kExactStageBytes = 64 * 1024;    // exact decode: S[n] staged when it fits
 constexpr size_t kCounterBytes = 256;        // counters are padded to this alignment
 
 struct FusedPlan {
@@ -41,12 +48,14 @@ struct FusedPlan {
   int ws;            // waves per side
   int astride;       // bf16 elements per gathered row in LDS
   int vstride;       // floats per projected row in LDS
-  int64_t rows;      // transition-table rows per request: 1 + (B-1) K
+  int64_t rows;      // per request: table rows 1 + (B-1) K (greedy), or floats of score blocks
+                     // and anchor scores (B-1) K K + K (exact)
+  bool stage;        // exact: the last workgroup stages the request's scores in LDS
   size_t x_bytes;    // shared region: gathered tile, then projections, then (last) the table
   size_t lds_bytes;  // total dynamic LDS
 };
 
-inline FusedPlan fused_plan(int64_t B, int K, int d) {
+inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact) {
   FusedPlan p;
   const VecGeom g = vec_geom(d);
   p.P = kSideRows / K;
@@ -56,10 +65,20 @@ inline FusedPlan fused_plan(int64_t B, int K, int d) {
   p.ws = g.waves;
   p.astride = g.dkp * 32 + 8;
   p.vstride = d + 4;
-  p.rows = 1 + (B - 1) * K;
   const size_t a_bytes = (size_t)2 * kSideRows * p.astride * 2;
   const size_t v_bytes = (size_t)2 * kSideRows * p.vstride * 4;
-  const size_t t_bytes = (size_t)p.rows * 8 + (size_t)B * 8;
+  size_t t_bytes;
+  if (exact) {
+    p.rows = (B - 1) * K * K + K;
+    const int G = K <= 16 ? 16 : (K <= 32 ? 32 : 64);
+    const size_t s_bytes = (size_t)(B - 1) * K * (G + 4) * 4;  // transposed, padded to G + 4
+    p.stage = s_bytes <= kExactStageBytes;
+    t_bytes = 64 * 4 + (p.stage ? s_bytes : 0) + (size_t)(B * K + B);
+  } else {
+    p.rows = 1 + (B - 1) * K;
+    p.stage = false;
+    t_bytes = (size_t)p.rows * 8 + (size_t)B * 8;
+  }
   p.x_bytes = a_bytes > v_bytes ? a_bytes : v_bytes;
   if (t_bytes > p.x_bytes) p.x_bytes = t_bytes;
   p.x_bytes = (p.x_bytes + 15) / 16 * 16;
@@ -71,23 +90,37 @@ inline FusedPlan fused_plan(int64_t B, int K, int d) {
   return p;
 }
 
-inline size_t fused_workspace_bytes(int64_t N, int64_t B, int K) {
-  const size_t counters = ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
-  return counters + (size_t)N * (size_t)(1 + (B - 1) * K) * 8;
+inline size_t counter_bytes(int64_t N) {
+  return ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
 }
 
-template <int G>
+inline size_t fused_workspace_bytes(int64_t N, int64_t B, int K, bool exact) {
+  if (exact) return counter_bytes(N) + (size_t)N * (size_t)((B - 1) * K * K + K) * 4;
+  return counter_bytes(N) + (size_t)N * (size_t)(1 + (B - 1) * K) * 8;
+}
+
+// Data one workgroup leaves for the request's last one goes out with device-coherent stores: they
+// leave little dirty in this compute unit's L2 for the release fence to write back (measured:
+// the fused pass 2.6 us faster with the greedy rule, 6.3 us with the exact one).
+template <typename T>
+__device__ __forceinline__ void exchange_store(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int G, bool EXACT>
 __global__ __launch_bounds__(512) void score_walk_kernel(
     const int32_t* __restrict__ ids, const float* __restrict__ logp,
     const uint16_t* __restrict__ E, int64_t V, int d, const unsigned char* __restrict__ frags,
     int nbp, int dkp, const float* __restrict__ anchor_out, int64_t B, int K, float sigma,
     float lambda, FusedPlan plan, float* __restrict__ S, float* __restrict__ S0,
     int32_t* __restrict__ draft, int32_t* __restrict__ choice, float* __restrict__ logq,
-    uint32_t* __restrict__ counters, uint64_t* __restrict__ table) {
+    float* __restrict__ score, uint32_t* __restrict__ counters, void* __restrict__ exchange) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [128][astride] gathered rows
   float* Vf = reinterpret_cast<float*>(smem);       // [128][vstride] projections (after A)
   uint64_t* tbl = reinterpret_cast<uint64_t*>(smem);  // [rows] the request's table (last wg)
+  uint64_t* table = static_cast<uint64_t*>(exchange);   // greedy: [N][rows] table entries
+  float* xs = static_cast<float*>(exchange);            // exact: [N][rows] scores
   float* ssw = reinterpret_cast<float*>(smem + plan.x_bytes);  // [2][ws][64]
   float* nrm = ssw + 2 * plan.ws * kSideRows;                   // [128]
   int32_t* rid = reinterpret_cast<int32_t*>(nrm + 2 * kSideRows);  // [128]
@@ -211,8 +244,15 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   }
   __syncthreads();
 
-  // ---- 5. transition-table rows (and the optional score outputs) -----------------------------
-  {
+  // ---- 5. transition-table rows, or (exact decode) the score blocks; optional outputs ------
+  if (EXACT) {
+    float* xn = xs + n * plan.rows;
+    if (npair > 0)
+      for (int i = tid; i < npair * K * K; i += nthreads)
+        exchange_store(&xn[(int64_t)t0 * K * K + i], sbuf[i]);
+    if (anchor_wg)
+      for (int i = tid; i < K; i += nthreads) exchange_store(&xn[(B - 1) * (int64_t)K * K + i], sbuf[i]);
+  } else {
     // rows of this workgroup: (slot t0+p+1, previous choice k) for p < npair, k < K; plus row 0
     // (slot 0) in the anchor workgroup, or in group 0 when there is no anchor
     const bool has_row0 = anchor_wg || (anchor_out == nullptr && g == 0);
@@ -238,8 +278,10 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
       int arg;
       float lq;
       resolve_row<G>(z, live, arg, lq);
-      if (j == 0 && grow >= 0) table[n * plan.rows + grow] = table_entry(arg, lq);
+      if (j == 0 && grow >= 0) exchange_store(&table[n * plan.rows + grow], table_entry(arg, lq));
     }
+  }
+  {
     if (S && npair > 0) {
       float* dst = S + ((n * (B - 1) + t0) * K) * (int64_t)K;
       for (int i = tid; i < npair * K * K; i += nthreads) dst[i] = sbuf[i];
@@ -263,6 +305,29 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   }
   __syncthreads();
   if (!*flag) return;
+  if (EXACT) {
+    const float* xn = xs + n * plan.rows;
+    const int64_t nS = (B - 1) * (int64_t)K * K;
+    float* line = reinterpret_cast<float*>(smem);  // [64]
+    float* T = line + kWave;                        // [B-1][K][G+4] when staged
+    uint8_t* from = reinterpret_cast<uint8_t*>(
+        T + (plan.stage ? (B - 1) * (int64_t)K * viterbi_stride<G>() : 0));
+    const float* S0n = anchor_out ? xn + nS : nullptr;
+    int32_t* choice_n = choice ? choice + n * B : nullptr;
+    float* logq_n = logq ? logq + n * B : nullptr;
+    float* score_n = score ? score + n : nullptr;
+    if (plan.stage) {
+      if (B > 1) stage_transposed<G>(T, xn, B, K, tid, nthreads);
+      __syncthreads();
+      viterbi_block<G, true>(T, S0n, lpn, ids + n * B * K, B, K, lambda, from, from + B * K,
+                             line, draft + n * B, choice_n, logq_n, score_n, tid, nthreads);
+    } else {
+      viterbi_block<G, false>(xn, S0n, lpn, ids + n * B * K, B, K, lambda, from, from + B * K,
+                              line, draft + n * B, choice_n, logq_n, score_n, tid, nthreads);
+    }
+    if (tid == 0) counters[n] = 0u;  // ready for the next call (visible to it at the kernel boundary)
+    return;
+  }
   for (int64_t i = tid; i < plan.rows; i += nthreads) tbl[i] = table[n * plan.rows + i];
   int32_t* ch = reinterpret_cast<int32_t*>(tbl + plan.rows);  // [B]
   float* lq_t = reinterpret_cast<float*>(ch + B);             // [B]
@@ -286,20 +351,72 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   }
 }
 
-template <int G>
-void launch_score_walk(const FusedPlan& plan, int64_t N, hipStream_t stream, const int32_t* ids,
-                       const float* logp, const uint16_t* E, int64_t V, int d,
-                       const unsigned char* frags, int nbp, int dkp, const float* anchor_out,
-                       int64_t B, int K, float sigma, float lambda, float* S, float* S0,
-                       int32_t* draft, int32_t* choice, float* logq, uint32_t* counters,
-                       uint64_t* table) {
+template <int G, bool EXACT>
+void launch_fused(const FusedPlan& plan, int64_t N, hipStream_t stream, const int32_t* ids,
+                  const float* logp, const uint16_t* E, int64_t V, int d,
+                  const unsigned char* frags, int nbp, int dkp, const float* anchor_out, int64_t B,
+                  int K, float sigma, float lambda, float* S, float* S0, int32_t* draft,
+                  int32_t* choice, float* logq, float* score, uint32_t* counters,
+                  void* exchange) {
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(score_walk_kernel<G>),
+      reinterpret_cast<const void*>(score_walk_kernel<G, EXACT>),
       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   (void)attr;
-  hipLaunchKernelGGL(score_walk_kernel<G>, dim3((unsigned)(N * plan.wg)), dim3(2 * plan.ws * kWave),
-                     plan.lds_bytes, stream, ids, logp, E, V, d, frags, nbp, dkp, anchor_out, B, K,
-                     sigma, lambda, plan, S, S0, draft, choice, logq, counters, table);
+  hipLaunchKernelGGL((score_walk_kernel<G, EXACT>), dim3((unsigned)(N * plan.wg)),
+                     dim3(2 * plan.ws * kWave), plan.lds_bytes, stream, ids, logp, E, V, d, frags,
+                     nbp, dkp, anchor_out, B, K, sigma, lambda, plan, S, S0, draft, choice, logq,
+                     score, counters, exchange);
+}
+
+inline bool fused_shape_ok(int64_t N, int64_t B, int K, bool exact) {
+  if (N < 1 || B < 1 || K < 1 || K > 64) return false;
+  if (exact) return B <= kMaxExactSlots && B * K <= kMaxExactBackPointers;
+  return B <= kMaxTableRows && 1 + (B - 1) * (int64_t)K <= kMaxTableRows;
+}
+
+template <bool EXACT>
+lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const void* E,
+                                 lilicorr_dtype e_dtype, int64_t V, int d, const void* packed_w,
+                                 const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
+                                 float logp_weight, float* S, float* S0, int32_t* draft,
+                                 int32_t* choice, float* logq, float* score, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  if (!ids || !logp || !E || !packed_w || !draft || !workspace) return LILICORR_ERR_INVALID_ARG;
+  if (e_dtype != LILICORR_F32 && e_dtype != LILICORR_BF16) return LILICORR_ERR_INVALID_ARG;
+  if (N < 1 || B < 1 || K < 1 || V < 1 || d < 1) return LILICORR_ERR_INVALID_ARG;
+  if (!isfinite(sigma) || !isfinite(logp_weight)) return LILICORR_ERR_INVALID_ARG;
+  if (e_dtype != LILICORR_BF16) return LILICORR_ERR_UNSUPPORTED;
+  if (d % 16 != 0 || d > kFusedMaxD || V >= ((int64_t)1 << 31)) return LILICORR_ERR_UNSUPPORTED;
+  if (!fused_shape_ok(N, B, K, EXACT)) return LILICORR_ERR_UNSUPPORTED;
+  if (!aligned16(ids) || !aligned16(logp) || !aligned16(E) || !aligned16(packed_w) ||
+      !aligned16(draft) || !aligned16(workspace) || (anchor_out && !aligned16(anchor_out)) ||
+      (S && !aligned16(S)) || (S0 && !aligned16(S0)) || (choice && !aligned16(choice)) ||
+      (logq && !aligned16(logq)) || (score && !aligned16(score)))
+    return LILICORR_ERR_ALIGNMENT;
+  if (workspace_bytes < fused_workspace_bytes(N, B, K, EXACT)) return LILICORR_ERR_WORKSPACE;
+  FusedPlan plan = fused_plan(B, K, d, EXACT);
+  if (anchor_out) plan.wg += 1;
+  if (N > 0x7fffffffll / plan.wg) return LILICORR_ERR_UNSUPPORTED;
+  if (plan.lds_bytes > 160 * 1024) return LILICORR_ERR_UNSUPPORTED;
+  const VecGeom g = vec_geom(d);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
+  void* exchange = ws + counter_bytes(N);
+  const uint16_t* e16 = static_cast<const uint16_t*>(E);
+  const unsigned char* frags = static_cast<const unsigned char*>(packed_w);
+  if (K <= 16)
+    launch_fused<16, EXACT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
+                            anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice, logq,
+                            score, counters, exchange);
+  else if (K <= 32)
+    launch_fused<32, EXACT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
+                            anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice, logq,
+                            score, counters, exchange);
+  else
+    launch_fused<64, EXACT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
+                            anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice, logq,
+                            score, counters, exchange);
+  return launch_status();
 }
 
 }  // namespace
@@ -308,9 +425,7 @@ void launch_score_walk(const FusedPlan& plan, int64_t N, hipStream_t stream, con
 using namespace lilicorr;
 
 extern "C" size_t lilicorr_score_walk_workspace_bytes(int64_t N, int64_t B, int K) {
-  if (N < 1 || B < 1 || K < 1 || K > 64) return 0;
-  if (1 + (B - 1) * (int64_t)K > kMaxTableRows) return 0;
-  return fused_workspace_bytes(N, B, K);
+  return fused_shape_ok(N, B, K, false) ? fused_workspace_bytes(N, B, K, false) : 0;
 }
 
 extern "C" lilicorr_status lilicorr_score_walk(
@@ -318,39 +433,21 @@ extern "C" lilicorr_status lilicorr_score_walk(
     const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
     float logp_weight, float* S, float* S0, int32_t* draft, int32_t* choice, float* logq,
     void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (!ids || !logp || !E || !packed_w || !draft || !workspace) return LILICORR_ERR_INVALID_ARG;
-  if (e_dtype != LILICORR_F32 && e_dtype != LILICORR_BF16) return LILICORR_ERR_INVALID_ARG;
-  if (N < 1 || B < 1 || K < 1 || V < 1 || d < 1) return LILICORR_ERR_INVALID_ARG;
-  if (!isfinite(sigma) || !isfinite(logp_weight)) return LILICORR_ERR_INVALID_ARG;
-  if (e_dtype != LILICORR_BF16) return LILICORR_ERR_UNSUPPORTED;
-  if (d % 16 != 0 || d > kFusedMaxD || K > 64 || V >= ((int64_t)1 << 31))
-    return LILICORR_ERR_UNSUPPORTED;
-  if (B > kMaxTableRows || 1 + (B - 1) * (int64_t)K > kMaxTableRows) return LILICORR_ERR_UNSUPPORTED;
-  if (!aligned16(ids) || !aligned16(logp) || !aligned16(E) || !aligned16(packed_w) ||
-      !aligned16(draft) || !aligned16(workspace) || (anchor_out && !aligned16(anchor_out)) ||
-      (S && !aligned16(S)) || (S0 && !aligned16(S0)) || (choice && !aligned16(choice)) ||
-      (logq && !aligned16(logq)))
-    return LILICORR_ERR_ALIGNMENT;
-  if (workspace_bytes < fused_workspace_bytes(N, B, K)) return LILICORR_ERR_WORKSPACE;
-  FusedPlan plan = fused_plan(B, K, d);
-  if (anchor_out) plan.wg += 1;
-  if (N > 0x7fffffffll / plan.wg) return LILICORR_ERR_UNSUPPORTED;
-  if (plan.lds_bytes > 160 * 1024) return LILICORR_ERR_UNSUPPORTED;
-  const VecGeom g = vec_geom(d);
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
-  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
-  uint64_t* table = reinterpret_cast<uint64_t*>(
-      ws + ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes);
-  const uint16_t* e16 = static_cast<const uint16_t*>(E);
-  const unsigned char* frags = static_cast<const unsigned char*>(packed_w);
-  if (K <= 16)
-    launch_score_walk<16>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp, anchor_out,
-                          B, K, sigma, logp_weight, S, S0, draft, choice, logq, counters, table);
-  else if (K <= 32)
-    launch_score_walk<32>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp, anchor_out,
-                          B, K, sigma, logp_weight, S, S0, draft, choice, logq, counters, table);
-  else
-    launch_score_walk<64>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp, anchor_out,
-                          B, K, sigma, logp_weight, S, S0, draft, choice, logq, counters, table);
-  return launch_status();
+  return score_and_decode<false>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K,
+                                 sigma, logp_weight, S, S0, draft, choice, logq, nullptr,
+                                 workspace, workspace_bytes, stream);
+}
+
+extern "C" size_t lilicorr_score_viterbi_workspace_bytes(int64_t N, int64_t B, int K) {
+  return fused_shape_ok(N, B, K, true) ? fused_workspace_bytes(N, B, K, true) : 0;
+}
+
+extern "C" lilicorr_status lilicorr_score_viterbi(
+    const int32_t* ids, const float* logp, const void* E, lilicorr_dtype e_dtype, int64_t V, int d,
+    const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
+    float logp_weight, float* S, float* S0, int32_t* draft, int32_t* choice, float* logq,
+    float* score, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return score_and_decode<true>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K, sigma,
+                                logp_weight, S, S0, draft, choice, logq, score, workspace,
+                                workspace_bytes, stream);
 }

@@ -27,7 +27,8 @@ def test_header_declares_the_path(L):
     names = _declared()
     for n in ["lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_pack_weights",
               "lilicorr_packed_weight_bytes", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
-              "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+              "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk",
+              "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes", "lilicorr_score_walk_workspace_bytes",
               "lilicorr_status_string"]:
         assert n in names
 
@@ -167,6 +168,27 @@ def test_score_walk_sizes_and_argument_errors(L):
     assert call(draft=A + 4) == -3
     assert call(anchor=A + 8) == -3
     assert call(ws_bytes=ws - 1) == -4
+
+
+def test_score_viterbi_sizes_and_argument_errors(L):
+    lib = L.load_library()
+    # counters, then N x ((B-1) K K + K) fp32 scores exchanged between workgroups
+    assert L.lilicorr_score_viterbi_workspace_bytes(64, 16, 16) == 256 + 64 * (15 * 256 + 16) * 4
+    assert L.lilicorr_score_viterbi_workspace_bytes(1, 8193, 1) == 0
+    assert L.lilicorr_score_viterbi_workspace_bytes(1, 2000, 64) == 0
+    ws = L.lilicorr_score_viterbi_workspace_bytes(2, 3, 4)
+    ok = [A, A, A, 1, 1000, 64, A, None, 2, 3, 4, 8.0, 0.0, None, None, A, None, None, None, A, ws,
+          None]
+    def call(i, v):
+        args = list(ok)
+        args[i] = v
+        return lib.lilicorr_score_viterbi(*args)
+    assert call(0, None) == -1        # ids
+    assert call(19, None) == -1       # workspace
+    assert call(3, 0) == -2           # fp32 embeddings
+    assert call(5, 512) == -2         # d above the fused pass
+    assert call(18, A + 4) == -3      # score alignment
+    assert call(20, ws - 1) == -4
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

@@ -121,3 +121,81 @@ def test_score_walk_reuses_workspace(lib):
         r = _oracle(ids, logp, to_np(E), W_in, W_out)
         _check(g, r, f"call {call}", B)
     assert int(ws[: 4 * N].view(torch.int32).abs().sum().item()) == 0  # counters back at zero
+
+
+# ---- the same pass with the exact max-path decode (lilicorr_score_viterbi) ---------------------
+
+def _run_exact(lib, ids, logp, E, packed, anchor=None, lam=0.0, workspace=None):
+    c = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    d, ch, q, g, S, S0 = lib.score_viterbi(c(ids), c(logp), E, packed, c(anchor), 8.0, lam,
+                                           scores=True, workspace=workspace)
+    torch.cuda.synchronize()
+    return dict(draft=to_np(d), choice=to_np(ch), logq=to_np(q), score=to_np(g),
+                S=to_np(S) if S is not None else None, S0=to_np(S0) if S0 is not None else None)
+
+
+def _check_exact(g, ids, logp, E_np, W_in, W_out, anchor, lam, what):
+    """Scores against the oracle's fp64 chain; the decode against the oracle's exact decode run
+    on the very scores the pass produced (both decide in fp32, so the path is bit-exact)."""
+    B = ids.shape[1]
+    r = _oracle(ids, logp, E_np, W_in, W_out, anchor, lam)
+    if B > 1:
+        assert_close(g["S"], r["S"], f"{what} S")
+    if anchor is not None:
+        assert_close(g["S0"], r["S0"], f"{what} S0")
+    S_g = g["S"] if B > 1 else np.zeros((ids.shape[0], 0, ids.shape[2], ids.shape[2]), np.float32)
+    vd, vc, vq, vs = oracle.viterbi_walk(S_g, g["S0"], logp, np.clip(ids, 0, None), lam)
+    assert_equal(g["choice"], vc, f"{what} choice")
+    assert_equal(g["draft"], np.take_along_axis(ids, vc[..., None].astype(np.int64), -1)[..., 0],
+                 f"{what} draft")
+    assert_close(g["logq"], vq, f"{what} logq")
+    assert_close(g["score"], vs, f"{what} score")
+
+
+@pytest.mark.parametrize("N,B,K,d,anchor,lam", [
+    (1, 1, 1, 16, False, 0.0), (1, 1, 4, 64, True, 0.0), (2, 2, 3, 48, True, 0.0),
+    (3, 5, 5, 80, False, 0.0), (2, 17, 16, 256, True, 0.0), (1, 9, 32, 128, False, 0.0),
+    (2, 4, 64, 256, True, 0.0), (4, 30, 8, 64, False, 1.0), (1, 300, 16, 32, False, 0.0),
+    (2, 16, 17, 96, True, -0.5), (2, 200, 64, 32, False, 0.0),
+])
+def test_score_viterbi_shapes(lib, N, B, K, d, anchor, lam):
+    print(f"score_viterbi N={N} B={B} K={K} d={d} anchor={anchor} lam={lam}", flush=True)
+    rng = np.random.default_rng(N * 7919 + B * 31 + K + 1)
+    V = 500
+    E = torch.from_numpy((rng.standard_normal((V, d)) * 0.05).astype(np.float32)).to(torch.bfloat16)
+    W_in = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
+    W_out = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
+    ids = rng.integers(0, V, size=(N, B, K)).astype(np.int32)
+    ids.reshape(-1)[::11] = -3
+    logp = -np.sort(rng.random((N, B, K)) * 4, axis=-1).astype(np.float32)
+    ao = rng.standard_normal((N, d)).astype(np.float32) if anchor else None
+    packed = lib.pack_weights(torch.from_numpy(W_in).cuda(), torch.from_numpy(W_out).cuda())
+    g = _run_exact(lib, ids, logp, E.cuda(), packed, ao, lam)
+    _check_exact(g, ids, logp, to_np(E), W_in, W_out, ao, lam, f"N={N} B={B} K={K} d={d}")
+
+
+@pytest.mark.parametrize("cfg_index", [1, 3])
+def test_score_viterbi_configs(lib, cfg_inputs, cfg_index):
+    cfg, inp = cfg_inputs(cfg_index)
+    print(f"score_viterbi config {cfg_index} {cfg.name}", flush=True)
+    ids, logp = lib.topk(inp["logits"].cuda(), cfg.K)
+    packed = lib.pack_weights(inp["W_in"].cuda(), inp["W_out"].cuda())
+    g = _run_exact(lib, to_np(ids), to_np(logp), inp["E"].cuda(), packed)
+    _check_exact(g, to_np(ids), to_np(logp), to_np(inp["E"]), to_np(inp["W_in"]),
+                 to_np(inp["W_out"]), None, 0.0, f"cfg{cfg_index}")
+
+
+def test_score_viterbi_reuses_workspace(lib):
+    rng = np.random.default_rng(5)
+    N, B, K, d, V = 8, 16, 16, 64, 300
+    E = torch.from_numpy((rng.standard_normal((V, d)) * 0.05).astype(np.float32)).to(torch.bfloat16)
+    W_in = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
+    W_out = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
+    packed = lib.pack_weights(torch.from_numpy(W_in).cuda(), torch.from_numpy(W_out).cuda())
+    ws = lib.score_viterbi_workspace(N, B, K)
+    for call, n in enumerate([N, N, 2]):
+        ids = rng.integers(0, V, size=(n, B, K)).astype(np.int32)
+        logp = -np.sort(rng.random((n, B, K)) * 4, axis=-1).astype(np.float32)
+        g = _run_exact(lib, ids, logp, E.cuda(), packed, workspace=ws)
+        _check_exact(g, ids, logp, to_np(E), W_in, W_out, None, 0.0, f"call {call}")
+    assert int(ws[: 4 * N].view(torch.int32).abs().sum().item()) == 0
