@@ -46,8 +46,9 @@ def _load():
         lib.oracle_pair_scores.argtypes = [P, P, P, I64, I64, I, I, ctypes.c_float, P, P]
         lib.oracle_greedy_walk.argtypes = [P, P, P, P, I64, I64, I, ctypes.c_float, P, P, P]
         lib.oracle_viterbi_walk.argtypes = [P, P, P, P, I64, I64, I, ctypes.c_float, P, P, P, P]
+        lib.oracle_candidate_features.argtypes = [P, I64, I, P]
         for f in (lib.oracle_topk, lib.oracle_candidate_vectors, lib.oracle_pair_scores,
-                  lib.oracle_greedy_walk, lib.oracle_viterbi_walk):
+                  lib.oracle_greedy_walk, lib.oracle_viterbi_walk, lib.oracle_candidate_features):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -146,3 +147,13 @@ def viterbi_walk(S: np.ndarray, S0, logp: np.ndarray, ids: np.ndarray, logp_weig
                                        float(logp_weight), _ptr(draft), _ptr(choice), _ptr(logq),
                                        _ptr(score)), "viterbi_walk")
     return draft, choice, logq, score
+
+
+def candidate_features(logp: np.ndarray) -> np.ndarray:
+    """logp [..., K] f32 (sorted top-K log-probabilities) -> feat [..., K, 5] f32."""
+    logp = np.ascontiguousarray(logp, dtype=np.float32)
+    K = logp.shape[-1]
+    rows = int(np.prod(logp.shape[:-1]))
+    feat = np.zeros(logp.shape + (5,), np.float32)
+    _check(_load().oracle_candidate_features(_ptr(logp), rows, K, _ptr(feat)), "candidate_features")
+    return feat

@@ -358,3 +358,31 @@ int oracle_viterbi_walk(const float *S, const float *S0, const float *logp, cons
     free(path);
     return 0;
 }
+
+/* ---------------------------------------------------------------------------------------------
+ * Candidate confidence features (implementation appendix, node construction): five scalars per
+ * candidate, read from the drafter's distribution at its slot. For candidate k (rank k, 0-based)
+ * of a row of K top-K log-probabilities logp[0..K-1] (sorted, rank 0 the most likely):
+ *     feat[k] = { logp[k], exp(logp[k]), logp[0] - logp[k], k / (K-1) (0 when K = 1), [k == 0] }
+ * Readings: the gap to the most likely token is taken as the non-negative difference, and the
+ * rank in [0, 1] as k / (K-1). Computed in double from the float log-probabilities.
+ * ------------------------------------------------------------------------------------------- */
+
+int oracle_candidate_features(const float *logp, int64_t rows, int K, float *feat)
+{
+    if (!logp || !feat || rows < 0 || K < 1)
+        return -1;
+    for (int64_t r = 0; r < rows; ++r) {
+        const double top = (double)logp[r * K];
+        for (int k = 0; k < K; ++k) {
+            const double lp = (double)logp[r * K + k];
+            float *f = feat + (r * K + k) * 5;
+            f[0] = (float)lp;
+            f[1] = (float)exp(lp);
+            f[2] = (float)(top - lp);
+            f[3] = K > 1 ? (float)((double)k / (double)(K - 1)) : 0.0f;
+            f[4] = k == 0 ? 1.0f : 0.0f;
+        }
+    }
+    return 0;
+}
