@@ -308,6 +308,11 @@ def main():
         print(f"[bench] stress logits generated in {time.perf_counter() - t:.1f} s", file=sys.stderr,
               flush=True)
         t3, m3, lo3, hi3 = time_logits_pass(L, torch, cfg, logits_list, iters=50, warmup=5)
+        feat = torch.empty(N, B, K, 5, dtype=torch.float32, device=dev)
+        feat_us = median_launch_us(torch, lambda: L.topk(
+            logits_list[0], K, out=(ids, logp, feat), workspace=ws, features=True))
+        plain_us = median_launch_us(torch, lambda: L.topk(logits_list[0], K, out=(ids, logp),
+                                                          workspace=ws))
         read3 = stream_read_rate(torch, logits_list)
         del logits_list
         torch.cuda.empty_cache()
@@ -318,7 +323,8 @@ def main():
             "headline": {"GB_s": algo_bytes / t3 / 1e9, "us": t3 * 1e6,
                          "us_median": m3 * 1e6, "us_p10": lo3 * 1e6, "us_p90": hi3 * 1e6,
                          "frac_of_8TBs": algo_bytes / t3 / 1e9 / PEAK_HBM_GBS,
-                         "stream_read_GB_s": read3},
+                         "stream_read_GB_s": read3,
+                         "with_features_us_median": feat_us, "same_buffer_us_median": plain_us},
             "stress": {"GB_s": b4 / t4 / 1e9, "us": t4 * 1e6,
                        "us_median": m4 * 1e6, "us_p10": lo4 * 1e6, "us_p90": hi4 * 1e6,
                        "frac_of_8TBs": b4 / t4 / 1e9 / PEAK_HBM_GBS,

@@ -70,6 +70,19 @@ lilicorr_status lilicorr_topk(const void *logits, lilicorr_dtype dtype, int64_t 
                               size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Step 1 with the candidates' confidence features: the same call as lilicorr_topk (same
+ * arguments, workspace and errors), plus, from the same pass over the logits,
+ *   feat   [N][B][K][5] fp32 out, the five scalars the head reads for each candidate
+ *          (implementation appendix, node construction), for the candidate at rank k of its slot:
+ *          { logp_k, exp(logp_k), logp_0 - logp_k, k / (K-1) (0 when K = 1), 1 if k == 0 else 0 }.
+ *          Required (not NULL), 16-byte aligned.
+ */
+lilicorr_status lilicorr_topk_features(const void *logits, lilicorr_dtype dtype, int64_t N,
+                                       int64_t B, int64_t V, int K, int32_t *ids, float *logp,
+                                       float *feat, void *workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
+/*
  * Step 2 — candidate in/out vectors. Each candidate carries an out vector and an in vector in
  * R^d, each normalised to unit L2 norm (Sec. 3.2; the two linear heads of the implementation
  * appendix). The trained head is out of reach here; its final linear heads are stood in for by

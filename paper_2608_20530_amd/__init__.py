@@ -3,6 +3,7 @@
 The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.h):
 
   lilicorr_topk               logits [N,B,V] -> ids, logp [N,B,K]       (Sec. 3.2; serving appendix)
+  lilicorr_topk_features      ... plus the five confidence scalars      (implementation appendix)
   lilicorr_pack_weights       W_in, W_out [d,d] -> matrix-core layout   (once per weight set)
   lilicorr_candidate_vectors  ids, E -> in_vec, out_vec [N,B,K,d]       (Sec. 3.2 unit-norm heads)
   lilicorr_pair_scores        in/out -> S [N,B-1,K,K] (+ S0 [N,K])      (Eq. pair)
@@ -24,7 +25,7 @@ import torch
 
 __all__ = [
     "LIB_PATH", "load_library", "LilicorrError", "SIGMA",
-    "lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
+    "lilicorr_topk", "lilicorr_topk_features", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
     "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
     "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes",
@@ -58,6 +59,7 @@ def load_library() -> ctypes.CDLL:
     sig = {
         "lilicorr_topk_workspace_bytes": ([I64, I64, I64, I], SZ),
         "lilicorr_topk": ([P, I, I64, I64, I64, I, P, P, P, SZ, P], I),
+        "lilicorr_topk_features": ([P, I, I64, I64, I64, I, P, P, P, P, SZ, P], I),
         "lilicorr_packed_weight_bytes": ([I], SZ),
         "lilicorr_pack_weights": ([P, P, I, P, P], I),
         "lilicorr_candidate_vectors": ([P, P, I, I64, I, P, I64, I64, I, P, P, P], I),
@@ -103,6 +105,12 @@ def lilicorr_packed_weight_bytes(d: int) -> int:
 
 def lilicorr_topk(logits, dtype, N, B, V, K, ids, logp, workspace, workspace_bytes, stream):
     return _call("lilicorr_topk", logits, dtype, N, B, V, K, ids, logp, workspace,
+                 workspace_bytes, stream)
+
+
+def lilicorr_topk_features(logits, dtype, N, B, V, K, ids, logp, feat, workspace, workspace_bytes,
+                           stream):
+    return _call("lilicorr_topk_features", logits, dtype, N, B, V, K, ids, logp, feat, workspace,
                  workspace_bytes, stream)
 
 
@@ -176,20 +184,28 @@ def _dtype_code(t: torch.Tensor) -> int:
     return BF16 if t.dtype == torch.bfloat16 else F32
 
 
-def topk(logits: torch.Tensor, K: int, *, out=None, workspace=None):
-    """logits [N,B,V] bf16/fp32 -> (ids [N,B,K] int32, logp [N,B,K] fp32)."""
+def topk(logits: torch.Tensor, K: int, *, out=None, workspace=None, features: bool = False):
+    """logits [N,B,V] bf16/fp32 -> (ids [N,B,K] int32, logp [N,B,K] fp32[, feat [N,B,K,5] fp32
+    when features=True])."""
     N, B, V = logits.shape
     dev = logits.device
     if out is None:
         out = (torch.empty(N, B, K, dtype=torch.int32, device=dev),
                torch.empty(N, B, K, dtype=torch.float32, device=dev))
-    ids, logp = out
+        if features:
+            out = out + (torch.empty(N, B, K, 5, dtype=torch.float32, device=dev),)
+    ids, logp = out[0], out[1]
     need = lilicorr_topk_workspace_bytes(N, B, V, K)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
-    lilicorr_topk(_dev(logits, "logits", (torch.bfloat16, torch.float32)), _dtype_code(logits),
-                  N, B, V, K, _dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)),
-                  _dev(workspace, "workspace"), workspace.numel(), _stream())
+    args = (_dev(logits, "logits", (torch.bfloat16, torch.float32)), _dtype_code(logits), N, B, V,
+            K, _dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)))
+    if features:
+        feat = out[2]
+        lilicorr_topk_features(*args, _dev(feat, "feat", (torch.float32,)),
+                               _dev(workspace, "workspace"), workspace.numel(), _stream())
+        return ids, logp, feat
+    lilicorr_topk(*args, _dev(workspace, "workspace"), workspace.numel(), _stream())
     return ids, logp
 
 

@@ -418,10 +418,33 @@ __device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K) 
   }
 }
 
+// Final outputs of a row from its merged sorted key list (one key per lane, lane 0 the best) and
+// its log-sum-exp: ids and log-probabilities, and when `feat` is given the five confidence
+// scalars of each candidate (implementation appendix): logp, p, the gap logp_top - logp, the rank
+// k / (K-1) in [0, 1] (0 when K = 1) and the top-choice indicator. Every lane calls it.
+__device__ __forceinline__ void write_row(uint64_t merged, double lse, int64_t row, int K,
+                                          int32_t* ids, float* logp, float* feat) {
+  const int lane = lane_id();
+  const double top = (double)key_value(readlane64(merged, 0)) - lse;
+  if (lane < K) {
+    const double lp = (double)key_value(merged) - lse;
+    ids[row * K + lane] = (int32_t)key_id(merged);
+    logp[row * K + lane] = (float)lp;
+    if (feat) {
+      float* f = feat + (row * K + lane) * 5;
+      f[0] = (float)lp;
+      f[1] = (float)exp(lp);
+      f[2] = (float)(top - lp);
+      f[3] = K > 1 ? (float)lane / (float)(K - 1) : 0.f;
+      f[4] = lane == 0 ? 1.f : 0.f;
+    }
+  }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
     const void* __restrict__ logits, int64_t V, int K, int split, int32_t* __restrict__ ids,
-    float* __restrict__ logp, unsigned char* __restrict__ partials) {
+    float* __restrict__ logp, float* __restrict__ feat, unsigned char* __restrict__ partials) {
   constexpr int EPC = ElemTraits<BF16>::kEPC;
   constexpr int U = kPerLane / EPC;
   constexpr int TILE = U * kWave;  // chunks per wave tile
@@ -551,11 +574,7 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
   const uint64_t merged = cons.L;
 
   if (split == 1) {
-    if (lane < K) {
-      const double lse = (log2((double)S) + (double)C) / (double)kLog2eF;
-      ids[row * K + lane] = (int32_t)key_id(merged);
-      logp[row * K + lane] = (float)((double)key_value(merged) - lse);
-    }
+    write_row(merged, (log2((double)S) + (double)C) / (double)kLog2eF, row, K, ids, logp, feat);
   } else {
     unsigned char* q = partials + ((size_t)row * split + part) * partial_stride(K);
     Partial* hdr = reinterpret_cast<Partial*>(q);
@@ -573,7 +592,8 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
 // One wave per row: merge the `split` partial results of the row.
 __global__ __launch_bounds__(kWave) void topk_merge_kernel(const unsigned char* __restrict__ partials,
                                                          int K, int split, int32_t* __restrict__ ids,
-                                                         float* __restrict__ logp) {
+                                                         float* __restrict__ logp,
+                                                         float* __restrict__ feat) {
   const int lane = lane_id();
   const int64_t row = blockIdx.x;
   uint64_t merged = 0;
@@ -595,11 +615,7 @@ __global__ __launch_bounds__(kWave) void topk_merge_kernel(const unsigned char* 
     uint64_t k = lane < K ? keys[lane] : 0ull;
     merged = p == 0 ? k : merge_desc64(merged, k);
   }
-  if (lane < K) {
-    double lse = (log2((double)S) + (double)C) / (double)kLog2eF;
-    ids[row * K + lane] = (int32_t)key_id(merged);
-    logp[row * K + lane] = (float)((double)key_value(merged) - lse);
-  }
+  write_row(merged, (log2((double)S) + (double)C) / (double)kLog2eF, row, K, ids, logp, feat);
 }
 
 // Number of workgroups per row: enough workgroups to fill the chip (about four per CU), but
@@ -636,15 +652,15 @@ extern "C" size_t lilicorr_topk_workspace_bytes(int64_t N, int64_t B, int64_t V,
   return (size_t)(N * B) * split * partial_stride(K);
 }
 
-extern "C" lilicorr_status lilicorr_topk(const void* logits, lilicorr_dtype dtype, int64_t N,
-                                         int64_t B, int64_t V, int K, int32_t* ids, float* logp,
-                                         void* workspace, size_t workspace_bytes,
-                                         hipStream_t stream) {
+static lilicorr_status topk_launch(const void* logits, lilicorr_dtype dtype, int64_t N, int64_t B,
+                                   int64_t V, int K, int32_t* ids, float* logp, float* feat,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!logits || !ids || !logp) return LILICORR_ERR_INVALID_ARG;
   if (dtype != LILICORR_F32 && dtype != LILICORR_BF16) return LILICORR_ERR_INVALID_ARG;
   if (!topk_args_ok(N, B, V, K)) return LILICORR_ERR_INVALID_ARG;
   if (K > 64 || K > V) return LILICORR_ERR_UNSUPPORTED;
-  if (!aligned16(logits) || !aligned16(ids) || !aligned16(logp)) return LILICORR_ERR_ALIGNMENT;
+  if (!aligned16(logits) || !aligned16(ids) || !aligned16(logp) || (feat && !aligned16(feat)))
+    return LILICORR_ERR_ALIGNMENT;
   const bool bf16 = dtype == LILICORR_BF16;
   const int64_t rows = N * B;
   const int split = topk_split(rows, V, bf16);
@@ -656,13 +672,34 @@ extern "C" lilicorr_status lilicorr_topk(const void* logits, lilicorr_dtype dtyp
   dim3 grid((unsigned)(rows * split)), block(kTopkWaves * kWave);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   if (bf16)
-    hipLaunchKernelGGL(topk_lse_kernel<true>, grid, block, 0, stream, logits, V, K, split, ids, logp, ws);
+    hipLaunchKernelGGL(topk_lse_kernel<true>, grid, block, 0, stream, logits, V, K, split, ids, logp,
+                       feat, ws);
   else
-    hipLaunchKernelGGL(topk_lse_kernel<false>, grid, block, 0, stream, logits, V, K, split, ids, logp, ws);
+    hipLaunchKernelGGL(topk_lse_kernel<false>, grid, block, 0, stream, logits, V, K, split, ids,
+                       logp, feat, ws);
   if (launch_status() != LILICORR_OK) return LILICORR_ERR_HIP;
   if (split > 1) {
-    hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)rows), dim3(kWave), 0, stream, ws, K, split, ids, logp);
+    hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)rows), dim3(kWave), 0, stream, ws, K, split,
+                       ids, logp, feat);
     if (launch_status() != LILICORR_OK) return LILICORR_ERR_HIP;
   }
   return LILICORR_OK;
+}
+
+extern "C" lilicorr_status lilicorr_topk(const void* logits, lilicorr_dtype dtype, int64_t N,
+                                         int64_t B, int64_t V, int K, int32_t* ids, float* logp,
+                                         void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream) {
+  return topk_launch(logits, dtype, N, B, V, K, ids, logp, nullptr, workspace, workspace_bytes,
+                     stream);
+}
+
+extern "C" lilicorr_status lilicorr_topk_features(const void* logits, lilicorr_dtype dtype,
+                                                  int64_t N, int64_t B, int64_t V, int K,
+                                                  int32_t* ids, float* logp, float* feat,
+                                                  void* workspace, size_t workspace_bytes,
+                                                  hipStream_t stream) {
+  if (!feat) return LILICORR_ERR_INVALID_ARG;
+  return topk_launch(logits, dtype, N, B, V, K, ids, logp, feat, workspace, workspace_bytes,
+                     stream);
 }

@@ -25,7 +25,7 @@ def L():
 
 def test_header_declares_the_path(L):
     names = _declared()
-    for n in ["lilicorr_topk", "lilicorr_topk_workspace_bytes", "lilicorr_pack_weights",
+    for n in ["lilicorr_topk", "lilicorr_topk_features", "lilicorr_topk_workspace_bytes", "lilicorr_pack_weights",
               "lilicorr_packed_weight_bytes", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
               "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk",
               "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes", "lilicorr_score_walk_workspace_bytes",
@@ -87,6 +87,19 @@ def test_topk_argument_errors(L):
     args = list(ok)
     args[2], args[3], args[4] = 1, 1, 151936
     assert lib.lilicorr_topk(*args) == -4
+
+
+def test_topk_features_argument_errors(L):
+    lib = L.load_library()
+    ok = [A, 1, 2, 3, 1000, 8, A, A, A, None, 0, None]
+    def call(i, v):
+        args = list(ok)
+        args[i] = v
+        return lib.lilicorr_topk_features(*args)
+    assert call(8, None) == -1          # feat is required
+    assert call(6, None) == -1          # ids
+    assert call(5, 65) == -2            # K > 64
+    assert call(8, A + 4) == -3         # feat alignment
 
 
 def test_other_argument_errors(L):

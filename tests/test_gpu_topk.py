@@ -119,3 +119,43 @@ def test_topk_rejects_bad_arguments(lib):
         lib.topk(x, 65)
     with pytest.raises(lib.LilicorrError):
         lib.topk(x, 0)
+
+
+# ---- confidence features from the same pass (lilicorr_topk_features) ---------------------------
+
+def _features(lib, logits_cpu, K):
+    ids, logp, feat = lib.topk(logits_cpu.cuda(), K, features=True)
+    torch.cuda.synchronize()
+    return to_np(ids), to_np(logp), to_np(feat)
+
+
+@pytest.mark.parametrize("cfg_index", [0, 1, 2, 3])
+def test_topk_features_configs(lib, cfg_inputs, cfg_index):
+    """ids / logp as lilicorr_topk gives them; features against the oracle's from its own logp
+    (configs 0-1 split each row over several workgroups: the merge kernel writes them)."""
+    cfg, inp = cfg_inputs(cfg_index)
+    print(f"features config {cfg_index} {cfg.name}", flush=True)
+    gi, gl, gf = _features(lib, inp["logits"], cfg.K)
+    ri, rl = lib.topk(inp["logits"].cuda(), cfg.K)
+    torch.cuda.synchronize()
+    assert_equal(gi, to_np(ri), "ids with and without features")
+    assert_equal(gl, to_np(rl), "logp with and without features")
+    if cfg.N <= 16:
+        oi, ol = oracle.topk(to_np(inp["logits"]), cfg.K)
+        assert_equal(gi, oi, "ids")
+        assert_close(gf, oracle.candidate_features(ol), "features")
+    else:  # the oracle's features from the GPU's log-probabilities (themselves checked above)
+        assert_close(gf, oracle.candidate_features(gl), "features")
+
+
+@pytest.mark.parametrize("K", [1, 3, 64])
+def test_topk_features_ties_and_small_k(lib, K):
+    g = torch.Generator().manual_seed(K)
+    x = torch.randn(2, 5, 3000, generator=g) * 3
+    x[:, :, 10:20] = x.max(-1, keepdim=True).values + 1.0  # ten-way tie at the top
+    xb = x.to(torch.bfloat16)
+    gi, gl, gf = _features(lib, xb, K)
+    oi, ol = oracle.topk(to_np(xb), K)
+    assert_equal(gi, oi, "ids")
+    assert_close(gf, oracle.candidate_features(ol), "features")
+    assert (gf[..., :min(K, 10), 2] == 0).all()  # tied with the top: zero gap
