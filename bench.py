@@ -279,6 +279,17 @@ def main():
                            "value": N * args.steps / sep_elapsed},
     }
 
+    # the same steps replayed from HIP graphs, one per rotating logits buffer
+    graphs = [L.BlockGraph(lg, K, E, packed) for lg in logits_list]
+    for i in range(args.warmup):
+        graphs[i % ROTATE].launch()
+    graph_elapsed = timed(lambda i: graphs[i % ROTATE].launch(), args.steps)
+    for gr in graphs:
+        gr.close()
+    out["graph_replay"] = {"path": "one HIP graph per block (lilicorr_block_graph_launch)",
+                           "ms_per_step": graph_elapsed / args.steps * 1e3,
+                           "value": N * args.steps / graph_elapsed}
+
     # the two decode rules of the decode-rule appendix, each in the fused pass and stand-alone,
     # on the candidates of the last timed step
     ws_exact = L.score_viterbi_workspace(N, B, K)
@@ -289,14 +300,22 @@ def main():
         ids, logp, E, packed, out=(draft, choice, logq), workspace=ws_fused))
     fused_exact = median_launch_us(torch, lambda: L.score_viterbi(
         ids, logp, E, packed, out=(draft, choice, logq, score), workspace=ws_exact))
+    ws_cert = L.score_walk_certified_workspace(N, B, K)
+    resc = torch.empty(N, B, dtype=torch.int32, device=dev)
+    fused_cert = median_launch_us(torch, lambda: L.score_walk_certified(
+        ids, logp, E, packed, out=(draft, choice, logq, resc), workspace=ws_cert))
     out["decode_rules"] = {
         "fused_greedy_us": fused_greedy,
+        "fused_certified_us": fused_cert,
+        "certified_rescored": int((resc > 0).sum()),
+        "certified_changed": int((resc == 2).sum()),
         "fused_exact_us": fused_exact,
         "greedy_walk_us": median_launch_us(torch, lambda: L.greedy_walk(
             S, None, logp, ids, 0.0, out=(draft, choice, logq))),
         "viterbi_walk_us": median_launch_us(torch, lambda: L.viterbi_walk(
             S, None, logp, ids, 0.0, out=(draft, choice, logq, score))),
         "step_us_greedy": topk_s * 1e6 + fused_greedy,
+        "step_us_certified": topk_s * 1e6 + fused_cert,
         "step_us_exact": topk_s * 1e6 + fused_exact,
         "note": "median call durations (HIP events); steps add the mean logits-pass launch",
     }

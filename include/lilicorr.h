@@ -16,7 +16,8 @@
  *    slot, V vocabulary size, d width of the in/out vectors.
  *  - Every call is asynchronous on `stream` (0 = the null stream) and allocates no memory;
  *    the library keeps no state between calls, so concurrent calls on different streams are safe
- *    when their outputs do not overlap.
+ *    when their outputs do not overlap. (The graph objects of lilicorr_block_graph_create are
+ *    the one exception: the caller creates and destroys them.)
  *  - Arguments are validated on the host before anything is launched: a negative status means
  *    nothing was launched and no output was written. LILICORR_ERR_HIP reports a failed launch.
  *  - Preconditions the library does not check (reading device data would cost a sync): logits
@@ -192,6 +193,39 @@ lilicorr_status lilicorr_score_walk(const int32_t *ids, const float *logp, const
                                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * lilicorr_score_walk with certified decisions. The greedy rule (Sec. 3.5) commits the candidate
+ * with the largest matching score of Eq. (pair); the pass computes those scores in fp32, whose
+ * error can reorder two nearly equal scores. Here every walk decision whose fp32 winner is
+ * within `margin` of another candidate is decided again from the definitions in double
+ * precision: each contender's u = e W (double, rows summed in order), v = u / ||u|| rounded to
+ * fp32, S = fp32(sigma * <o, i> / (||o|| ||i||)) with the sums over the fp32 vectors in index
+ * order, z = S (+ logp_weight * logp, one fp32 rounding), then the lowest index among the
+ * largest z. Every step is a correctly rounded IEEE double operation in a fixed order, so the
+ * decision equals that of a plain double-precision evaluation of the same formulas whenever the
+ * fp32 scores are within margin / 2 of those values.
+ *   margin       fp32 score gap at or below which a decision is re-scored; finite and >= 0.
+ *   S, S0        as for lilicorr_score_walk; entries of re-scored contenders hold the
+ *                re-scored values.
+ *   logq         as for lilicorr_score_walk; for a re-scored decision the pass's value moved by
+ *                the re-scored difference between the new and the fp32 winner.
+ *   rescored     [N][B] int32 out or NULL: 0 decision not re-scored, 1 re-scored and unchanged,
+ *                2 re-scored and changed from the fp32 winner. 16-byte aligned.
+ *   workspace    lilicorr_score_walk_certified_workspace_bytes(N, B, K) bytes, zero-filled once,
+ *                as for lilicorr_score_walk.
+ * Other arguments, limits and errors as for lilicorr_score_walk; the fp32 weights come from the
+ * packed buffer's copy. LILICORR_ERR_INVALID_ARG for a negative or non-finite margin.
+ */
+size_t lilicorr_score_walk_certified_workspace_bytes(int64_t N, int64_t B, int K);
+lilicorr_status lilicorr_score_walk_certified(const int32_t *ids, const float *logp, const void *E,
+                                              lilicorr_dtype e_dtype, int64_t V, int d,
+                                              const void *packed_w, const float *anchor_out,
+                                              int64_t N, int64_t B, int K, float sigma,
+                                              float logp_weight, float margin, float *S,
+                                              float *S0, int32_t *draft, int32_t *choice,
+                                              float *logq, int32_t *rescored, void *workspace,
+                                              size_t workspace_bytes, hipStream_t stream);
+
+/*
  * The same single pass with the exact max-path decode in place of the greedy walk (the decode-rule
  * appendix serves each rule as one fused kernel): the draft, choice, logq and score that
  * lilicorr_candidate_vectors -> lilicorr_pair_scores -> lilicorr_viterbi_walk give on the same
@@ -208,6 +242,63 @@ lilicorr_status lilicorr_score_viterbi(const int32_t *ids, const float *logp, co
                                        float *S0, int32_t *draft, int32_t *choice, float *logq,
                                        float *score, void *workspace, size_t workspace_bytes,
                                        hipStream_t stream);
+
+/*
+ * One draft block as one HIP graph (implementation appendix, serving: candidate extraction,
+ * matching and selection replayed as one graph per block). lilicorr_block_graph_create records
+ * lilicorr_topk followed by one fused pass (greedy, certified greedy or exact decode) with the
+ * arguments below, on a stream of its own, without running anything; every replay then runs the
+ * block on whatever the buffers hold at that time. The graph keeps the pointers: the buffers
+ * must stay allocated, at the same addresses, until the graph is destroyed, and replays that
+ * share buffers must not overlap in time. Unlike the calls above, create allocates the graph's
+ * host-side objects (no device buffers); launch and destroy allocate nothing.
+ * Errors: any status the recorded calls would return for these arguments (nothing is recorded
+ * then and *graph is NULL), LILICORR_ERR_INVALID_ARG for a NULL args or graph pointer or an
+ * unknown decode, LILICORR_ERR_HIP if capture or instantiation fails.
+ */
+typedef enum {
+    LILICORR_DECODE_GREEDY = 0,    /* lilicorr_score_walk */
+    LILICORR_DECODE_CERTIFIED = 1, /* lilicorr_score_walk_certified */
+    LILICORR_DECODE_EXACT = 2,     /* lilicorr_score_viterbi */
+} lilicorr_decode;
+
+typedef struct {
+    /* step 1, as for lilicorr_topk */
+    const void *logits;
+    lilicorr_dtype logits_dtype;
+    int64_t N, B, V;
+    int K;
+    int32_t *ids;
+    float *logp;
+    void *topk_workspace;
+    size_t topk_workspace_bytes;
+    /* steps 2-4, as for the fused pass `decode` names (e_rows is that call's V: rows of E) */
+    const void *E;
+    lilicorr_dtype e_dtype;
+    int64_t e_rows;
+    int d;
+    const void *packed_w;
+    const float *anchor_out;
+    float sigma, logp_weight;
+    lilicorr_decode decode;
+    float margin;       /* certified only */
+    float *S, *S0;      /* optional */
+    int32_t *draft, *choice;
+    float *logq;
+    float *score;       /* exact only, optional */
+    int32_t *rescored;  /* certified only, optional */
+    void *fused_workspace;
+    size_t fused_workspace_bytes;
+} lilicorr_block_args;
+
+typedef struct lilicorr_graph lilicorr_graph;
+
+lilicorr_status lilicorr_block_graph_create(const lilicorr_block_args *args,
+                                            lilicorr_graph **graph);
+/* Replays the block on `stream` (asynchronous, as every call above). */
+lilicorr_status lilicorr_block_graph_launch(lilicorr_graph *graph, hipStream_t stream);
+/* Releases the graph (NULL is ignored); the caller makes sure no replay is still running. */
+void lilicorr_block_graph_destroy(lilicorr_graph *graph);
 
 /* Static, human-readable name of a status code. */
 const char *lilicorr_status_string(lilicorr_status s);

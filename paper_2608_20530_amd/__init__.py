@@ -10,7 +10,9 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
   lilicorr_greedy_walk        S, S0, logp, ids -> draft, choice, logq   (Sec. 3.5, Eq. localar)
   lilicorr_viterbi_walk       S, S0, logp, ids -> best path, logq, g    (Eq. pathscore)
   lilicorr_score_walk         ids, logp, E -> draft, choice, logq       (steps 2-4 in one pass)
+  lilicorr_score_walk_certified  the same pass, near-tied decisions decided again in fp64
   lilicorr_score_viterbi      the same pass with the exact max-path decode
+  lilicorr_block_graph_*      top-K + one fused pass recorded as one HIP graph, replayed per block
 
 This module only marshals arguments: torch supplies device memory and the current HIP stream,
 and every step of the path runs in the library's kernels. There is no fallback: if the library
@@ -28,22 +30,46 @@ __all__ = [
     "lilicorr_topk", "lilicorr_topk_features", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
     "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+    "lilicorr_score_walk_certified", "lilicorr_score_walk_certified_workspace_bytes",
     "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes",
-    "lilicorr_status_string",
+    "lilicorr_block_graph_create", "lilicorr_block_graph_launch", "lilicorr_block_graph_destroy",
+    "BlockArgs", "BlockGraph", "lilicorr_status_string",
     "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk", "score_viterbi",
-    "draft_block",
+    "score_walk_certified", "score_walk_certified_workspace", "CERT_MARGIN", "draft_block",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblilicorr.so")
 SIGMA = 8.0  # cosine scale of Eq. (pair), hyper-parameter table of the implementation appendix
+# fp32 score gap at or below which score_walk_certified decides again in fp64; the certificate
+# holds while every fp32 node score is within CERT_MARGIN / 2 (3.1e-5) of its double-precision
+# value, and the fused pass's fp32 pair scores measure within 1.8e-6 of it on the workloads
+CERT_MARGIN = 2.0 ** -14
 
 F32, BF16 = 0, 1
+DECODE = {"greedy": 0, "certified": 1, "exact": 2}
 
 _lib = None
 
 
 class LilicorrError(RuntimeError):
     pass
+
+
+class BlockArgs(ctypes.Structure):
+    """lilicorr_block_args of include/lilicorr.h, field for field."""
+    _fields_ = [
+        ("logits", ctypes.c_void_p), ("logits_dtype", ctypes.c_int),
+        ("N", ctypes.c_int64), ("B", ctypes.c_int64), ("V", ctypes.c_int64), ("K", ctypes.c_int),
+        ("ids", ctypes.c_void_p), ("logp", ctypes.c_void_p), ("topk_workspace", ctypes.c_void_p),
+        ("topk_workspace_bytes", ctypes.c_size_t),
+        ("E", ctypes.c_void_p), ("e_dtype", ctypes.c_int), ("e_rows", ctypes.c_int64),
+        ("d", ctypes.c_int), ("packed_w", ctypes.c_void_p), ("anchor_out", ctypes.c_void_p),
+        ("sigma", ctypes.c_float), ("logp_weight", ctypes.c_float), ("decode", ctypes.c_int),
+        ("margin", ctypes.c_float), ("S", ctypes.c_void_p), ("S0", ctypes.c_void_p),
+        ("draft", ctypes.c_void_p), ("choice", ctypes.c_void_p), ("logq", ctypes.c_void_p),
+        ("score", ctypes.c_void_p), ("rescored", ctypes.c_void_p),
+        ("fused_workspace", ctypes.c_void_p), ("fused_workspace_bytes", ctypes.c_size_t),
+    ]
 
 
 def load_library() -> ctypes.CDLL:
@@ -69,9 +95,15 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_score_walk_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_walk": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, SZ,
                                  P], I),
+        "lilicorr_score_walk_certified_workspace_bytes": ([I64, I64, I], SZ),
+        "lilicorr_score_walk_certified": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, F, P, P, P,
+                                           P, P, P, P, SZ, P], I),
         "lilicorr_score_viterbi_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_viterbi": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, P,
                                     SZ, P], I),
+        "lilicorr_block_graph_create": ([ctypes.POINTER(BlockArgs), ctypes.POINTER(P)], I),
+        "lilicorr_block_graph_launch": ([P, P], I),
+        "lilicorr_block_graph_destroy": ([P], None),
         "lilicorr_status_string": ([I], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -150,6 +182,18 @@ def lilicorr_score_walk(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
                  stream)
 
 
+def lilicorr_score_walk_certified_workspace_bytes(N: int, B: int, K: int) -> int:
+    return int(load_library().lilicorr_score_walk_certified_workspace_bytes(N, B, K))
+
+
+def lilicorr_score_walk_certified(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K,
+                                  sigma, logp_weight, margin, S, S0, draft, choice, logq, rescored,
+                                  workspace, workspace_bytes, stream):
+    return _call("lilicorr_score_walk_certified", ids, logp, E, e_dtype, V, d, packed_w,
+                 anchor_out, N, B, K, sigma, logp_weight, margin, S, S0, draft, choice, logq,
+                 rescored, workspace, workspace_bytes, stream)
+
+
 def lilicorr_score_viterbi_workspace_bytes(N: int, B: int, K: int) -> int:
     return int(load_library().lilicorr_score_viterbi_workspace_bytes(N, B, K))
 
@@ -160,6 +204,21 @@ def lilicorr_score_viterbi(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N,
     return _call("lilicorr_score_viterbi", ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N,
                  B, K, sigma, logp_weight, S, S0, draft, choice, logq, score, workspace,
                  workspace_bytes, stream)
+
+
+def lilicorr_block_graph_create(args: BlockArgs) -> int:
+    """-> the graph handle (an integer address); raises on a non-zero status."""
+    handle = ctypes.c_void_p()
+    _call("lilicorr_block_graph_create", ctypes.byref(args), ctypes.byref(handle))
+    return handle.value
+
+
+def lilicorr_block_graph_launch(graph, stream):
+    return _call("lilicorr_block_graph_launch", graph, stream)
+
+
+def lilicorr_block_graph_destroy(graph) -> None:
+    load_library().lilicorr_block_graph_destroy(graph)
 
 
 # ---- torch conveniences (marshalling only) -----------------------------------------------------
@@ -329,6 +388,50 @@ def score_walk(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor, packed: t
     return draft, choice, logq
 
 
+def score_walk_certified_workspace(N: int, B: int, K: int, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace for score_walk_certified (kept zeroed between calls)."""
+    need = lilicorr_score_walk_certified_workspace_bytes(N, B, K)
+    if need == 0:
+        raise LilicorrError(f"score_walk_certified does not support N={N}, B={B}, K={K}")
+    return torch.zeros(need, dtype=torch.uint8, device=device)
+
+
+def score_walk_certified(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor,
+                         packed: torch.Tensor, anchor_out=None, sigma: float = SIGMA,
+                         logp_weight: float = 0.0, margin: float = CERT_MARGIN, *,
+                         scores: bool = False, out=None, workspace=None):
+    """Steps 2-4 in one pass, near-tied decisions re-scored in fp64 -> (draft, choice, logq,
+    rescored[, S, S0 when scores=True])."""
+    N, B, K = ids.shape
+    V, d = E.shape
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.float32, device=dev),
+               torch.empty(N, B, dtype=torch.int32, device=dev))
+    draft, choice, logq, rescored = out
+    S = S0 = None
+    if scores:
+        S = torch.empty(N, max(B - 1, 0), K, K, dtype=torch.float32, device=dev)
+        S0 = torch.empty(N, K, dtype=torch.float32, device=dev) if anchor_out is not None else None
+    if workspace is None:
+        workspace = score_walk_certified_workspace(N, B, K, dev)
+    lilicorr_score_walk_certified(
+        _dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)),
+        _dev(E, "E", (torch.bfloat16, torch.float32)), _dtype_code(E), V, d,
+        _dev(packed, "packed"), _dev(anchor_out, "anchor_out", (torch.float32,)), N, B, K,
+        float(sigma), float(logp_weight), float(margin),
+        _dev(S, "S", (torch.float32,)) if S is not None and B > 1 else None,
+        _dev(S0, "S0", (torch.float32,)), _dev(draft, "draft", (torch.int32,)),
+        _dev(choice, "choice", (torch.int32,)), _dev(logq, "logq", (torch.float32,)),
+        _dev(rescored, "rescored", (torch.int32,)), _dev(workspace, "workspace"),
+        workspace.numel(), _stream())
+    if scores:
+        return draft, choice, logq, rescored, S, S0
+    return draft, choice, logq, rescored
+
+
 def score_viterbi_workspace(N: int, B: int, K: int, device="cuda") -> torch.Tensor:
     """A zero-filled workspace for score_viterbi (the library keeps it zeroed between calls)."""
     need = lilicorr_score_viterbi_workspace_bytes(N, B, K)
@@ -370,6 +473,85 @@ def score_viterbi(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor, packed
     if scores:
         return draft, choice, logq, score, S, S0
     return draft, choice, logq, score
+
+
+class BlockGraph:
+    """One draft block (top-K, then one fused pass) recorded as a HIP graph over fixed buffers.
+
+    The outputs (ids, logp, draft, choice, logq, and score / rescored / S / S0 where they apply)
+    are allocated here; launch() replays the block on the current stream over whatever `logits`
+    holds then. The object keeps every buffer the graph points at alive until close().
+    """
+
+    def __init__(self, logits: torch.Tensor, K: int, E: torch.Tensor, packed: torch.Tensor,
+                 anchor_out=None, sigma: float = SIGMA, logp_weight: float = 0.0,
+                 decode: str = "greedy", margin: float = CERT_MARGIN, scores: bool = False):
+        if decode not in DECODE:
+            raise LilicorrError(f"unknown decode {decode!r}; one of {sorted(DECODE)}")
+        N, B, V = logits.shape
+        rows, d = E.shape
+        dev = logits.device
+        self.logits, self.E, self.packed, self.anchor_out = logits, E, packed, anchor_out
+        self.ids = torch.empty(N, B, K, dtype=torch.int32, device=dev)
+        self.logp = torch.empty(N, B, K, dtype=torch.float32, device=dev)
+        need = lilicorr_topk_workspace_bytes(N, B, V, K)
+        self.topk_workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+        self.draft = torch.empty(N, B, dtype=torch.int32, device=dev)
+        self.choice = torch.empty(N, B, dtype=torch.int32, device=dev)
+        self.logq = torch.empty(N, B, dtype=torch.float32, device=dev)
+        self.score = (torch.empty(N, dtype=torch.float32, device=dev) if decode == "exact"
+                      else None)
+        self.rescored = (torch.empty(N, B, dtype=torch.int32, device=dev)
+                         if decode == "certified" else None)
+        self.S = self.S0 = None
+        if scores:
+            self.S = torch.empty(N, max(B - 1, 0), K, K, dtype=torch.float32, device=dev)
+            self.S0 = (torch.empty(N, K, dtype=torch.float32, device=dev)
+                       if anchor_out is not None else None)
+        ws_fn = {"greedy": score_walk_workspace, "certified": score_walk_certified_workspace,
+                 "exact": score_viterbi_workspace}[decode]
+        self.fused_workspace = ws_fn(N, B, K, dev)
+        a = BlockArgs()
+        a.logits = _dev(logits, "logits", (torch.bfloat16, torch.float32))
+        a.logits_dtype = _dtype_code(logits)
+        a.N, a.B, a.V, a.K = N, B, V, K
+        a.ids, a.logp = self.ids.data_ptr(), self.logp.data_ptr()
+        a.topk_workspace = self.topk_workspace.data_ptr()
+        a.topk_workspace_bytes = self.topk_workspace.numel()
+        a.E = _dev(E, "E", (torch.bfloat16, torch.float32))
+        a.e_dtype = _dtype_code(E)
+        a.e_rows, a.d = rows, d
+        a.packed_w = _dev(packed, "packed")
+        a.anchor_out = _dev(anchor_out, "anchor_out", (torch.float32,))
+        a.sigma, a.logp_weight = float(sigma), float(logp_weight)
+        a.decode, a.margin = DECODE[decode], float(margin)
+        a.S = self.S.data_ptr() if self.S is not None and B > 1 else None
+        a.S0 = self.S0.data_ptr() if self.S0 is not None else None
+        a.draft, a.choice, a.logq = (self.draft.data_ptr(), self.choice.data_ptr(),
+                                     self.logq.data_ptr())
+        a.score = self.score.data_ptr() if self.score is not None else None
+        a.rescored = self.rescored.data_ptr() if self.rescored is not None else None
+        a.fused_workspace = self.fused_workspace.data_ptr()
+        a.fused_workspace_bytes = self.fused_workspace.numel()
+        self.args = a
+        self._graph = lilicorr_block_graph_create(a)
+
+    def launch(self) -> None:
+        if self._graph is None:
+            raise LilicorrError("the graph was closed")
+        lilicorr_block_graph_launch(self._graph, _stream())
+
+    def close(self) -> None:
+        """Releases the graph; the caller makes sure no replay is still running."""
+        if self._graph is not None:
+            lilicorr_block_graph_destroy(self._graph)
+            self._graph = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def draft_block(logits: torch.Tensor, K: int, E: torch.Tensor, packed: torch.Tensor,

@@ -234,17 +234,24 @@ __device__ __forceinline__ float group_allreduce(float v, Op op) {
 // group holds z_j; lanes with live == false hold no candidate): the lowest j attaining max z
 // (0 if none does, which only NaN scores cause) and the local log-likelihood
 // -log sum_j exp(z_j - max z) of Eq. (localar), both in fp32. Every lane of the wave must call it.
+// m receives the row's maximum.
 template <int G>
-__device__ __forceinline__ void resolve_row(float z, bool live, int& arg, float& lq) {
+__device__ __forceinline__ void resolve_row(float z, bool live, int& arg, float& lq, float& m) {
   const int gshift = (lane_id() / G) * G;  // first ballot bit of this lane's group
   const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
-  const float m = group_allreduce<G>(live ? z : -__builtin_inff(),
-                                     [](float a, float b) { return fmaxf(a, b); });
+  m = group_allreduce<G>(live ? z : -__builtin_inff(),
+                         [](float a, float b) { return fmaxf(a, b); });
   const uint64_t hits = (__ballot(live && z == m) >> gshift) & gmask;
   arg = hits ? __ffsll((long long)hits) - 1 : 0;
   const float s = group_allreduce<G>(live ? expf(z - m) : 0.f,
                                      [](float a, float b) { return a + b; });
   lq = -logf(s);
+}
+
+template <int G>
+__device__ __forceinline__ void resolve_row(float z, bool live, int& arg, float& lq) {
+  float m;
+  resolve_row<G>(z, live, arg, lq, m);
 }
 
 // table entry: low 32 bits the argmax, high 32 bits the fp32 local log-likelihood

@@ -20,10 +20,14 @@
 // The exact max-path variant (decode-rule appendix) replaces steps 5-6: every workgroup writes its
 // score blocks to the workspace and the request's last workgroup runs the dynamic program over
 // all of them (viterbi_block), as the paper serves both decode rules as one fused kernel each.
+// The certified greedy variant flags, in step 5, every row whose fp32 winner is within a margin
+// of another candidate and records the contenders; in step 6 the last workgroup decides each
+// flagged row it meets on the path again in double precision (certify.hpp).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
 
+#include "certify.hpp"
 #include "common.hpp"
 #include "lilicorr.h"
 #include "projection.hpp"
@@ -51,12 +55,14 @@ struct FusedPlan {
   int64_t rows;      // per request: table rows 1 + (B-1) K (greedy), or floats of score blocks
                      // and anchor scores (B-1) K K + K (exact)
   bool stage;        // exact: the last workgroup stages the request's scores in LDS
+  size_t cert_off;   // certified greedy: offset of the re-scoring scratch in the shared region
   size_t x_bytes;    // shared region: gathered tile, then projections, then (last) the table
   size_t lds_bytes;  // total dynamic LDS
 };
 
-inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact) {
+inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = false) {
   FusedPlan p;
+  p.cert_off = 0;
   const VecGeom g = vec_geom(d);
   p.P = kSideRows / K;
   const int64_t pairs = B - 1;
@@ -77,7 +83,12 @@ inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact) {
   } else {
     p.rows = 1 + (B - 1) * K;
     p.stage = false;
-    t_bytes = (size_t)p.rows * 8 + (size_t)B * 8;
+    // table, then per slot: choice, logq (and the re-scoring mark when certified)
+    t_bytes = (size_t)p.rows * 8 + (size_t)B * (cert ? 12 : 8);
+    if (cert) {
+      p.cert_off = (t_bytes + 15) / 16 * 16;
+      t_bytes = p.cert_off + cert_scratch_bytes(d, 2 * p.ws * kWave);
+    }
   }
   p.x_bytes = a_bytes > v_bytes ? a_bytes : v_bytes;
   if (t_bytes > p.x_bytes) p.x_bytes = t_bytes;
@@ -94,9 +105,11 @@ inline size_t counter_bytes(int64_t N) {
   return ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
 }
 
-inline size_t fused_workspace_bytes(int64_t N, int64_t B, int K, bool exact) {
+// counters, then the exchange region: score blocks (exact), or table entries and, when
+// certified, one contender mask per table row
+inline size_t fused_workspace_bytes(int64_t N, int64_t B, int K, bool exact, bool cert = false) {
   if (exact) return counter_bytes(N) + (size_t)N * (size_t)((B - 1) * K * K + K) * 4;
-  return counter_bytes(N) + (size_t)N * (size_t)(1 + (B - 1) * K) * 8;
+  return counter_bytes(N) + (size_t)N * (size_t)(1 + (B - 1) * K) * 8 * (cert ? 2 : 1);
 }
 
 // Data one workgroup leaves for the request's last one goes out with device-coherent stores: they
@@ -107,14 +120,16 @@ __device__ __forceinline__ void exchange_store(T* p, T v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int G, bool EXACT>
+template <int G, bool EXACT, bool CERT>
 __global__ __launch_bounds__(512) void score_walk_kernel(
     const int32_t* __restrict__ ids, const float* __restrict__ logp,
     const uint16_t* __restrict__ E, int64_t V, int d, const unsigned char* __restrict__ frags,
     int nbp, int dkp, const float* __restrict__ anchor_out, int64_t B, int K, float sigma,
     float lambda, FusedPlan plan, float* __restrict__ S, float* __restrict__ S0,
     int32_t* __restrict__ draft, int32_t* __restrict__ choice, float* __restrict__ logq,
-    float* __restrict__ score, uint32_t* __restrict__ counters, void* __restrict__ exchange) {
+    float* __restrict__ score, uint32_t* __restrict__ counters, void* __restrict__ exchange,
+    float margin, const float* __restrict__ w32, uint64_t* __restrict__ cmask,
+    int32_t* __restrict__ rescored) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [128][astride] gathered rows
   float* Vf = reinterpret_cast<float*>(smem);       // [128][vstride] projections (after A)
@@ -276,9 +291,23 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
       }
       if (lr < nrows) grow = lr < npair * K ? 1 + (int64_t)t0 * K + lr : 0;
       int arg;
-      float lq;
-      resolve_row<G>(z, live, arg, lq);
-      if (j == 0 && grow >= 0) exchange_store(&table[n * plan.rows + grow], table_entry(arg, lq));
+      float lq, m;
+      resolve_row<G>(z, live, arg, lq, m);
+      uint32_t lo = (uint32_t)arg;
+      uint64_t cont = 0;
+      if (CERT) {
+        // contenders: every candidate within the margin of the fp32 maximum. Row 0 without an
+        // anchor needs none: its scores are lambda * logp (or 0) on both sides of any comparison.
+        const int gshift = (lane / G) * G;
+        const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
+        cont = (__ballot(live && z >= m - margin) >> gshift) & gmask;
+        if ((lr < npair * K || anchor_wg) && __popcll(cont) > 1) lo |= kCertFlag;
+      }
+      if (j == 0 && grow >= 0) {
+        exchange_store(&table[n * plan.rows + grow],
+                       (uint64_t)lo | ((uint64_t)__float_as_uint(lq) << 32));
+        if (CERT && (lo & kCertFlag)) exchange_store(&cmask[n * plan.rows + grow], cont);
+      }
     }
   }
   {
@@ -331,8 +360,43 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   for (int64_t i = tid; i < plan.rows; i += nthreads) tbl[i] = table[n * plan.rows + i];
   int32_t* ch = reinterpret_cast<int32_t*>(tbl + plan.rows);  // [B]
   float* lq_t = reinterpret_cast<float*>(ch + B);             // [B]
+  int32_t* rs_t = reinterpret_cast<int32_t*>(lq_t + B);       // [B] (certified)
   __syncthreads();
-  if (tid == 0) {
+  if (CERT) {
+    // every thread follows the table (same entries, so the same branches); a flagged row on the
+    // path is decided again by the whole workgroup
+    const float* w_in = w32;
+    const float* w_out = w32 + (size_t)d * d;
+    const int32_t* idn = ids + n * B * K;
+    int c = 0;
+    for (int64_t t = 0; t < B; ++t) {
+      const int64_t row = t == 0 ? 0 : 1 + (t - 1) * K + c;
+      const uint64_t e = tbl[row];
+      int arg = (int)((uint32_t)e & kArgMask);
+      float lq = __uint_as_float((uint32_t)(e >> 32));
+      int mark = 0;
+      if ((uint32_t)e & kCertFlag) {
+        float dlq;
+        const int best = certify_decision(
+            t == 0 ? anchor_out + n * d : nullptr, t == 0 ? -1 : idn[(t - 1) * K + c],
+            idn + t * K, lpn + t * K, cmask[n * plan.rows + row], arg, E, V, d, w_in, w_out,
+            sigma, lambda,
+            t == 0 ? (S0 ? S0 + n * K : nullptr)
+                   : (S ? S + ((n * (B - 1) + t - 1) * K + c) * (int64_t)K : nullptr),
+            smem + plan.cert_off, tid, nthreads, dlq);
+        mark = best == arg ? 1 : 2;
+        arg = best;
+        lq += dlq;
+      }
+      if (tid == 0) {
+        ch[t] = arg;
+        lq_t[t] = lq;
+        rs_t[t] = mark;
+      }
+      c = arg;
+    }
+    if (tid == 0) counters[n] = 0u;  // ready for the next call (visible to it at the kernel boundary)
+  } else if (tid == 0) {
     int c = 0;
     for (int64_t t = 0; t < B; ++t) {
       const uint64_t e = tbl[t == 0 ? 0 : 1 + (t - 1) * K + c];
@@ -348,24 +412,34 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
     draft[n * B + t] = ids[(n * B + t) * K + ct];
     if (choice) choice[n * B + t] = ct;
     if (logq) logq[n * B + t] = lq_t[t];
+    if (CERT && rescored) rescored[n * B + t] = rs_t[t];
   }
 }
 
-template <int G, bool EXACT>
+// certified greedy decode only: the re-scoring margin, the fp32 weights (the packed buffer's
+// copy), the contender masks in the workspace, the optional re-scoring marks
+struct CertArgs {
+  float margin;
+  const float* w32;
+  uint64_t* cmask;
+  int32_t* rescored;
+};
+
+template <int G, bool EXACT, bool CERT>
 void launch_fused(const FusedPlan& plan, int64_t N, hipStream_t stream, const int32_t* ids,
                   const float* logp, const uint16_t* E, int64_t V, int d,
                   const unsigned char* frags, int nbp, int dkp, const float* anchor_out, int64_t B,
                   int K, float sigma, float lambda, float* S, float* S0, int32_t* draft,
                   int32_t* choice, float* logq, float* score, uint32_t* counters,
-                  void* exchange) {
+                  void* exchange, const CertArgs& ca) {
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(score_walk_kernel<G, EXACT>),
+      reinterpret_cast<const void*>(score_walk_kernel<G, EXACT, CERT>),
       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   (void)attr;
-  hipLaunchKernelGGL((score_walk_kernel<G, EXACT>), dim3((unsigned)(N * plan.wg)),
+  hipLaunchKernelGGL((score_walk_kernel<G, EXACT, CERT>), dim3((unsigned)(N * plan.wg)),
                      dim3(2 * plan.ws * kWave), plan.lds_bytes, stream, ids, logp, E, V, d, frags,
                      nbp, dkp, anchor_out, B, K, sigma, lambda, plan, S, S0, draft, choice, logq,
-                     score, counters, exchange);
+                     score, counters, exchange, ca.margin, ca.w32, ca.cmask, ca.rescored);
 }
 
 inline bool fused_shape_ok(int64_t N, int64_t B, int K, bool exact) {
@@ -374,27 +448,30 @@ inline bool fused_shape_ok(int64_t N, int64_t B, int K, bool exact) {
   return B <= kMaxTableRows && 1 + (B - 1) * (int64_t)K <= kMaxTableRows;
 }
 
-template <bool EXACT>
+template <bool EXACT, bool CERT>
 lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const void* E,
                                  lilicorr_dtype e_dtype, int64_t V, int d, const void* packed_w,
                                  const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
-                                 float logp_weight, float* S, float* S0, int32_t* draft,
-                                 int32_t* choice, float* logq, float* score, void* workspace,
-                                 size_t workspace_bytes, hipStream_t stream) {
+                                 float logp_weight, float margin, float* S, float* S0,
+                                 int32_t* draft, int32_t* choice, float* logq, float* score,
+                                 int32_t* rescored, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
   if (!ids || !logp || !E || !packed_w || !draft || !workspace) return LILICORR_ERR_INVALID_ARG;
   if (e_dtype != LILICORR_F32 && e_dtype != LILICORR_BF16) return LILICORR_ERR_INVALID_ARG;
   if (N < 1 || B < 1 || K < 1 || V < 1 || d < 1) return LILICORR_ERR_INVALID_ARG;
   if (!isfinite(sigma) || !isfinite(logp_weight)) return LILICORR_ERR_INVALID_ARG;
+  if (CERT && !(isfinite(margin) && margin >= 0.f)) return LILICORR_ERR_INVALID_ARG;
   if (e_dtype != LILICORR_BF16) return LILICORR_ERR_UNSUPPORTED;
   if (d % 16 != 0 || d > kFusedMaxD || V >= ((int64_t)1 << 31)) return LILICORR_ERR_UNSUPPORTED;
   if (!fused_shape_ok(N, B, K, EXACT)) return LILICORR_ERR_UNSUPPORTED;
   if (!aligned16(ids) || !aligned16(logp) || !aligned16(E) || !aligned16(packed_w) ||
       !aligned16(draft) || !aligned16(workspace) || (anchor_out && !aligned16(anchor_out)) ||
       (S && !aligned16(S)) || (S0 && !aligned16(S0)) || (choice && !aligned16(choice)) ||
-      (logq && !aligned16(logq)) || (score && !aligned16(score)))
+      (logq && !aligned16(logq)) || (score && !aligned16(score)) ||
+      (rescored && !aligned16(rescored)))
     return LILICORR_ERR_ALIGNMENT;
-  if (workspace_bytes < fused_workspace_bytes(N, B, K, EXACT)) return LILICORR_ERR_WORKSPACE;
-  FusedPlan plan = fused_plan(B, K, d, EXACT);
+  if (workspace_bytes < fused_workspace_bytes(N, B, K, EXACT, CERT)) return LILICORR_ERR_WORKSPACE;
+  FusedPlan plan = fused_plan(B, K, d, EXACT, CERT);
   if (anchor_out) plan.wg += 1;
   if (N > 0x7fffffffll / plan.wg) return LILICORR_ERR_UNSUPPORTED;
   if (plan.lds_bytes > 160 * 1024) return LILICORR_ERR_UNSUPPORTED;
@@ -404,18 +481,23 @@ lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const vo
   void* exchange = ws + counter_bytes(N);
   const uint16_t* e16 = static_cast<const uint16_t*>(E);
   const unsigned char* frags = static_cast<const unsigned char*>(packed_w);
+  CertArgs ca{margin, nullptr, nullptr, rescored};
+  if (CERT) {
+    ca.w32 = reinterpret_cast<const float*>(frags + frag_bytes(d));
+    ca.cmask = static_cast<uint64_t*>(exchange) + N * plan.rows;
+  }
   if (K <= 16)
-    launch_fused<16, EXACT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
-                            anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice, logq,
-                            score, counters, exchange);
+    launch_fused<16, EXACT, CERT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
+                                  anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice,
+                                  logq, score, counters, exchange, ca);
   else if (K <= 32)
-    launch_fused<32, EXACT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
-                            anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice, logq,
-                            score, counters, exchange);
+    launch_fused<32, EXACT, CERT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
+                                  anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice,
+                                  logq, score, counters, exchange, ca);
   else
-    launch_fused<64, EXACT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
-                            anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice, logq,
-                            score, counters, exchange);
+    launch_fused<64, EXACT, CERT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
+                                  anchor_out, B, K, sigma, logp_weight, S, S0, draft, choice,
+                                  logq, score, counters, exchange, ca);
   return launch_status();
 }
 
@@ -433,9 +515,23 @@ extern "C" lilicorr_status lilicorr_score_walk(
     const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
     float logp_weight, float* S, float* S0, int32_t* draft, int32_t* choice, float* logq,
     void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return score_and_decode<false>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K,
-                                 sigma, logp_weight, S, S0, draft, choice, logq, nullptr,
-                                 workspace, workspace_bytes, stream);
+  return score_and_decode<false, false>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
+                                        K, sigma, logp_weight, 0.f, S, S0, draft, choice, logq,
+                                        nullptr, nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" size_t lilicorr_score_walk_certified_workspace_bytes(int64_t N, int64_t B, int K) {
+  return fused_shape_ok(N, B, K, false) ? fused_workspace_bytes(N, B, K, false, true) : 0;
+}
+
+extern "C" lilicorr_status lilicorr_score_walk_certified(
+    const int32_t* ids, const float* logp, const void* E, lilicorr_dtype e_dtype, int64_t V, int d,
+    const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
+    float logp_weight, float margin, float* S, float* S0, int32_t* draft, int32_t* choice,
+    float* logq, int32_t* rescored, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return score_and_decode<false, true>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K,
+                                       sigma, logp_weight, margin, S, S0, draft, choice, logq,
+                                       nullptr, rescored, workspace, workspace_bytes, stream);
 }
 
 extern "C" size_t lilicorr_score_viterbi_workspace_bytes(int64_t N, int64_t B, int K) {
@@ -447,7 +543,7 @@ extern "C" lilicorr_status lilicorr_score_viterbi(
     const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
     float logp_weight, float* S, float* S0, int32_t* draft, int32_t* choice, float* logq,
     float* score, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  return score_and_decode<true>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K, sigma,
-                                logp_weight, S, S0, draft, choice, logq, score, workspace,
-                                workspace_bytes, stream);
+  return score_and_decode<true, false>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K,
+                                       sigma, logp_weight, 0.f, S, S0, draft, choice, logq, score,
+                                       nullptr, workspace, workspace_bytes, stream);
 }

@@ -29,7 +29,9 @@ def test_header_declares_the_path(L):
               "lilicorr_packed_weight_bytes", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
               "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk",
               "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes", "lilicorr_score_walk_workspace_bytes",
-              "lilicorr_status_string"]:
+              "lilicorr_score_walk_certified", "lilicorr_score_walk_certified_workspace_bytes",
+              "lilicorr_block_graph_create", "lilicorr_block_graph_launch",
+              "lilicorr_block_graph_destroy", "lilicorr_status_string"]:
         assert n in names
 
 
@@ -181,6 +183,70 @@ def test_score_walk_sizes_and_argument_errors(L):
     assert call(draft=A + 4) == -3
     assert call(anchor=A + 8) == -3
     assert call(ws_bytes=ws - 1) == -4
+
+
+def test_score_walk_certified_sizes_and_argument_errors(L):
+    lib = L.load_library()
+    # counters, the table rows, then one 8-byte contender mask per table row
+    assert L.lilicorr_score_walk_certified_workspace_bytes(64, 16, 16) == 256 + 64 * 241 * 16
+    assert L.lilicorr_score_walk_certified_workspace_bytes(2, 3, 4) == 256 + 2 * 9 * 16
+    assert L.lilicorr_score_walk_certified_workspace_bytes(1, 2, 65) == 0
+    ws = L.lilicorr_score_walk_certified_workspace_bytes(2, 3, 4)
+    names = ["ids", "logp", "E", "e_dtype", "V", "d", "packed", "anchor", "N", "B", "K", "sigma",
+             "lw", "margin", "S", "S0", "draft", "choice", "logq", "rescored", "ws", "ws_bytes",
+             "stream"]
+    ok = [A, A, A, 1, 1000, 64, A, None, 2, 3, 4, 8.0, 0.0, 2.0 ** -14, None, None, A, None, None,
+          None, A, ws, None]
+    def call(**kw):
+        args = list(ok)
+        for k, v in kw.items():
+            args[names.index(k)] = v
+        return lib.lilicorr_score_walk_certified(*args)
+    assert call(ids=None) == -1
+    assert call(ws=None) == -1
+    assert call(margin=-1.0) == -1
+    assert call(margin=float("nan")) == -1
+    assert call(margin=float("inf")) == -1
+    assert call(e_dtype=0) == -2
+    assert call(d=512) == -2
+    assert call(rescored=A + 4) == -3
+    assert call(ws_bytes=ws - 1) == -4
+    # the plain pass's workspace is too small for the contender masks
+    assert call(ws_bytes=L.lilicorr_score_walk_workspace_bytes(2, 3, 4)) == -4
+
+
+def test_block_args_layout_matches_the_header(L, tmp_path):
+    """The binding's BlockArgs has the C struct's size and field offsets (compiled with gcc)."""
+    import ctypes
+    import subprocess
+
+    fields = [f for f, _ in L.BlockArgs._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"lilicorr.h\"\n"
+                   "int main(void) {\n"
+                   "  printf(\"%zu\\n\", sizeof(lilicorr_block_args));\n" +
+                   "".join(f"  printf(\"%zu\\n\", offsetof(lilicorr_block_args, {f}));\n"
+                           for f in fields) + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c11", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+                           "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)])
+    got = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert got[0] == ctypes.sizeof(L.BlockArgs)
+    assert got[1:] == [getattr(L.BlockArgs, f).offset for f in fields]
+
+
+def test_block_graph_argument_errors(L):
+    import ctypes
+    lib = L.load_library()
+    handle = ctypes.c_void_p(123)
+    assert lib.lilicorr_block_graph_create(None, ctypes.byref(handle)) == -1
+    a = L.BlockArgs()
+    assert lib.lilicorr_block_graph_create(ctypes.byref(a), None) == -1
+    a.decode = 7
+    assert lib.lilicorr_block_graph_create(ctypes.byref(a), ctypes.byref(handle)) == -1
+    assert handle.value is None                 # set to NULL on every error
+    assert lib.lilicorr_block_graph_launch(None, None) == -1
+    lib.lilicorr_block_graph_destroy(None)      # ignored
 
 
 def test_score_viterbi_sizes_and_argument_errors(L):
