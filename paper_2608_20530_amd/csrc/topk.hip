@@ -4,24 +4,29 @@
 //
 // Design (gfx950), one workgroup per row segment, four waves:
 //  * Three producer waves stream the logits from HBM exactly once with 16-byte non-temporal
-//    buffer loads, in interleaved tiles of 64 lanes x 32 elements (4 KB of bf16), two tiles in
-//    flight per wave.
+//    buffer loads, in interleaved tiles of 64 lanes x 32 elements (4 KB of bf16); each wave
+//    issues its next tile's loads before it processes the current one.
 //  * Log-sum-exp: every element adds exp2(x*log2e - c) to a per-lane partial sum; c is a
 //    wave-uniform integer reference (log2 units), so moving it only rescales the partial sums by
 //    an exact power of two. c follows the top-K threshold value (a logit of the row, so the
 //    maximum's term stays at or above 2^-1) and is raised to the tile maximum in the rare case
 //    a tile sum exceeds 2^64.
-//  * Top-K: a wave-uniform threshold key T (published in LDS) screens each tile. bf16 tiles are
-//    screened with packed 16-bit integer max on the raw bit patterns, so a tile with no candidate
-//    costs about half an instruction per element. The screen is strict (x > value of T) whenever
-//    every id in the tile exceeds T's id, which keeps runs of exactly tied logits out. Elements
-//    whose full (value, id) key beats T are pushed, with ballot + mbcnt, into a single-producer
-//    ring in LDS.
-//  * The fourth wave is the consumer: it drains the rings, keeps the one sorted list of the
-//    row's K best keys in registers (one key per lane, insertion by DPP lane shift, or a bitonic
-//    sort + merge for large batches) and publishes the list's K-th key as the new threshold. The
-//    serial list work thus never stalls the HBM stream. Each producer seeds the threshold from
+//  * Top-K: a wave-uniform threshold key T (published in LDS) screens every 16-byte chunk of a
+//    tile. bf16 chunks are screened with packed 16-bit integer max on the raw bit patterns (five
+//    instructions per 8 elements). The screen is strict (x > value of T) whenever every id in the
+//    tile exceeds T's id, which keeps runs of exactly tied logits out. A chunk that passes is
+//    copied whole, with its first id and a mask of its real elements, into the producer's
+//    single-producer ring in LDS (one 16-byte and one 8-byte store, slots assigned by ballot +
+//    mbcnt): the producer never branches per element, which keeps its vector issue, the bound of
+//    this kernel, on the stream.
+//  * The fourth wave is the consumer, at raised issue priority: it drains the rings, drops chunks
+//    whose maximum has fallen below the current threshold, expands the rest into (value, id) keys
+//    and keeps the one sorted list of the row's K best keys in registers (one key per lane,
+//    insertion by DPP lane shift, or a bitonic sort + merge when many keys arrive at once); it
+//    publishes the list's K-th key as the new threshold. Each producer seeds the threshold from
 //    its first tile with the K-th largest lane maximum (radix select across lanes).
+//  * Every value the screen derives from T (strictness, the integer bound, the exp reference) is
+//    wave-uniform and kept in scalar registers, so the per-tile control flow is scalar branches.
 //  * Rows split over several workgroups (small N*B) write partial results to the workspace and a
 //    second kernel merges them.
 #include <hip/hip_runtime.h>
@@ -39,7 +44,7 @@ constexpr int kPerLane = 32;                         // elements per lane per ti
 constexpr int kRebase = 16;                          // max term exponent before the reference moves
 constexpr int kTopkWaves = 4;                        // wave 0 consumes, waves 1..3 produce
 constexpr int kProducers = kTopkWaves - 1;
-constexpr uint32_t kRing = 512;                      // keys per producer ring (power of two)
+constexpr uint32_t kRing = 256;                      // staged chunks per producer ring (power of two)
 constexpr int kSpinLimit = 1 << 22;                  // bound on any wait (never reached)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -66,6 +71,15 @@ struct ElemTraits<false> {
   static constexpr int kEPC = 4;
 };
 
+// A staged chunk: one lane's 16 bytes of logits that may hold a candidate, with the row-relative
+// id of its first element and a mask of the elements that belong to the row segment.
+struct StagedChunk {
+  u32x4 raw;
+  uint32_t id0;
+  uint32_t mask;
+  uint32_t pad[2];
+};
+
 struct TopkShared {
   uint64_t T;                      // best published threshold key (atomic max)
   uint32_t tail[kProducers];       // ring write positions (producer-owned)
@@ -74,7 +88,7 @@ struct TopkShared {
   int cref[kProducers];
   int cvalid[kProducers];
   float s[kProducers];
-  uint64_t ring[kProducers][kRing];
+  StagedChunk ring[kProducers][kRing];
 };
 
 __device__ __forceinline__ uint64_t atomic_load_T(TopkShared& sh) {
@@ -155,26 +169,28 @@ __device__ __forceinline__ void unpack_tile(const u32x4 (&raw)[kPerLane / ElemTr
   }
 }
 
-// 1 if the tile may hold an element >= Tv (> Tv when strict), for a positive bf16-representable
-// Tv: positive bf16 bit patterns order like signed 16-bit integers, and every negative pattern
-// (including the -inf padding) is below them. Packed 16-bit max over the raw tile.
-template <bool STRICT>
-__device__ __forceinline__ int bf16_screen(const u32x4 (&raw)[4], float Tv) {
+// Largest bf16 value of a 16-byte chunk (8 elements), as the signed 16-bit integer of its bit
+// pattern: for positive values the integer order is the value order, and every negative pattern
+// (including the -inf padding) sorts below every positive one. Packed 16-bit max over the chunk.
+__device__ __forceinline__ int bf16_chunk_max(const u32x4& r) {
   // (each dword is copied to a scalar before the bit cast: a bit cast applied directly to a
   // vector element subscript has been seen to read element 0)
-  const uint32_t w00 = raw[0][0];
-  i16x2 m = __builtin_bit_cast(i16x2, w00);
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (u || q) {
-        const uint32_t w = raw[u][q];
-        m = __builtin_elementwise_max(m, __builtin_bit_cast(i16x2, w));
-      }
-  const int mx = m[0] > m[1] ? (int)m[0] : (int)m[1];
-  const int tb = (int)(__float_as_uint(Tv) >> 16);
-  return STRICT ? (mx > tb ? 1 : 0) : (mx >= tb ? 1 : 0);
+  const uint32_t w0 = r[0], w1 = r[1], w2 = r[2], w3 = r[3];
+  const i16x2 m = __builtin_elementwise_max(
+      __builtin_elementwise_max(__builtin_bit_cast(i16x2, w0), __builtin_bit_cast(i16x2, w1)),
+      __builtin_elementwise_max(__builtin_bit_cast(i16x2, w2), __builtin_bit_cast(i16x2, w3)));
+  return m[0] > m[1] ? (int)m[0] : (int)m[1];
+}
+
+// Element e of a 16-byte chunk as fp32.
+template <bool BF16>
+__device__ __forceinline__ float chunk_elem(const u32x4& r, int e) {
+  if (BF16) {
+    const uint32_t d = r[e >> 1];
+    return __uint_as_float((e & 1) ? (d & 0xffff0000u) : (d << 16));
+  }
+  const uint32_t d = r[e];
+  return __uint_as_float(d);
 }
 
 // ---- producer ---------------------------------------------------------------------------------
@@ -199,10 +215,10 @@ __device__ __forceinline__ void rebase(Producer& pr, int need) {
   }
 }
 
-// Append the keys of the lanes with `live` set to this producer's ring.
-__device__ __forceinline__ void push_keys(Producer& pr, TopkShared& sh, uint64_t key, bool live) {
-  const uint64_t m = __ballot(live);
-  if (!m) return;
+// Copy the chunks of the lanes with `live` set into this producer's ring (one 16-byte and one
+// 8-byte LDS store per lane), waiting for ring space if the consumer is behind.
+__device__ __forceinline__ void stage_chunks(Producer& pr, TopkShared& sh, const u32x4& r,
+                                             uint32_t id0, uint32_t mask, bool live, uint64_t m) {
   const uint32_t n = (uint32_t)__popcll(m);
   if (pr.tail + n - pr.head > kRing) {
     // make everything written so far visible to the consumer before waiting for it
@@ -216,9 +232,16 @@ __device__ __forceinline__ void push_keys(Producer& pr, TopkShared& sh, uint64_t
   }
   if (live) {
     const uint32_t off = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    sh.ring[pr.p][(pr.tail + off) & (kRing - 1)] = key;
+    StagedChunk& e = sh.ring[pr.p][(pr.tail + off) & (kRing - 1)];
+    e.raw = r;
+    *reinterpret_cast<uint2*>(&e.id0) = make_uint2(id0, mask);
   }
   pr.tail += n;
+}
+
+__device__ __forceinline__ void publish_tail(Producer& pr, TopkShared& sh) {
+  if (lane_id() == 0)
+    __hip_atomic_store(&sh.tail[pr.p], pr.tail, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // The K-th largest lane maximum of a tile bounds the row's K-th largest element from below:
@@ -240,89 +263,40 @@ __device__ __forceinline__ bool strict_ok(uint64_t T, uint32_t tile_min_id) {
   return T != 0 && key_id(T) < tile_min_id;
 }
 
-// Push every element of the tile whose key beats T, scanning only the 8-element blocks that reach
-// tv (strict: x > tv, else x >= tv; see strict_ok).
-template <bool STRICT, int NE, typename IdOf, typename ValidOf>
-__device__ __forceinline__ void push_tile(Producer& pr, TopkShared& sh, const float (&x)[NE],
-                                          IdOf id_of, ValidOf valid_of, float tv, uint64_t T) {
-  constexpr int NB = (NE + 7) / 8;
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    float bm = -__builtin_inff();
-#pragma unroll
-    for (int j = 8 * b; j < 8 * b + 8 && j < NE; ++j) bm = fmaxf(bm, x[j]);
-    if (!__ballot(STRICT ? (bm > tv) : (bm >= tv))) continue;
-#pragma unroll
-    for (int j = 8 * b; j < 8 * b + 8 && j < NE; ++j) {
-      const bool pred = STRICT ? (x[j] > tv) : (x[j] >= tv);
-      if (!__ballot(pred)) continue;
-      const uint64_t kj = make_key(x[j], id_of(j));
-      push_keys(pr, sh, kj, pred && valid_of(j) && kj > T);
-    }
-  }
+// The producer's current threshold: the consumer's published key or this producer's own seed.
+__device__ __forceinline__ uint64_t producer_T(const Producer& pr, TopkShared& sh) {
+  const uint64_t T = atomic_load_T(sh);
+  return uniform64(pr.seedT > T ? pr.seedT : T);
 }
 
-// One tile of NE elements per lane. x[] are the values; id_of(j) gives the row-relative token id
-// of element j of this lane and valid_of(j) whether it is a real element (tiles are padded with
-// -inf). raw, when not null, is the tile's raw bf16 data for the packed screen; tile_min_id is
-// the smallest id in the tile (0: never screen strictly).
-template <int NE, typename IdOf, typename ValidOf>
-__device__ __forceinline__ void produce_tile(Producer& pr, TopkShared& sh, const float (&x)[NE],
-                                             const u32x4* raw, IdOf id_of, ValidOf valid_of, int K,
-                                             bool first, uint32_t tile_min_id) {
-  const int lane = lane_id();
-  uint64_t T = atomic_load_T(sh);
-  if (pr.seedT > T) T = pr.seedT;
+// Seed this producer's threshold from its first tile (lane maxima of the tile).
+__device__ __forceinline__ uint64_t seed_from(Producer& pr, TopkShared& sh, uint64_t T,
+                                              float lane_max, int K) {
+  const uint64_t seedT = uniform64(seed_threshold(lane_max, K));
+  if (key_value(seedT) > -__builtin_inff() && seedT > T) {
+    // a bound for the whole row: the K lanes behind it hold K distinct elements at or above it
+    pr.seedT = seedT;
+    publish_T(sh, seedT);
+    return seedT;
+  }
+  return T;
+}
+
+// Exp sums of NE elements per lane. The reference follows the threshold value (an element's
+// value, so never above the row maximum); an element far above it shows up as a tile sum beyond
+// 2^kBig (or inf), and the tile is then summed again with the reference at the tile maximum.
+template <int NE>
+__device__ __forceinline__ void exp_accumulate(Producer& pr, const float (&x)[NE], uint64_t T) {
+  // T is wave-uniform: the reference is computed on the vector unit and read back as a scalar
+  if (T != 0) rebase(pr, (int)uniform32((uint32_t)ref_for(key_value(T))));
   float lane_max = -__builtin_inff();
   bool have_max = false;
-  if (first) {
+  if (!pr.cvalid) {
 #pragma unroll
     for (int j = 0; j < NE; ++j) lane_max = fmaxf(lane_max, x[j]);
     have_max = true;
-    const uint64_t seedT = uniform64(seed_threshold(lane_max, K));
-    if (key_value(seedT) > -__builtin_inff() && seedT > T) {
-      // a bound for the whole row: the K lanes behind it hold K distinct elements at or above it
-      pr.seedT = seedT;
-      T = seedT;
-      publish_T(sh, seedT);
-    }
-  }
-  const float tv = key_value(T);
-  const bool strict = strict_ok(T, tile_min_id);
-  int flag;
-  if (raw != nullptr && !first && tv > 0.f) {
-    const u32x4(&r4)[4] = *reinterpret_cast<const u32x4(*)[4]>(raw);
-    flag = strict ? bf16_screen<true>(r4, tv) : bf16_screen<false>(r4, tv);
-  } else {
-    if (!have_max) {
-#pragma unroll
-      for (int j = 0; j < NE; ++j) lane_max = fmaxf(lane_max, x[j]);
-      have_max = true;
-    }
-    flag = strict ? (lane_max > tv) : (lane_max >= tv);
-  }
-
-  if (__ballot(flag != 0)) {
-    if (strict)
-      push_tile<true>(pr, sh, x, id_of, valid_of, tv, T);
-    else
-      push_tile<false>(pr, sh, x, id_of, valid_of, tv, T);
-    if (lane == 0)
-      __hip_atomic_store(&sh.tail[pr.p], pr.tail, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-  }
-
-  // Exp sums. The reference follows the threshold value (an element's value, so never above the
-  // row maximum); an element far above it shows up as a tile sum beyond 2^kBig (or inf), and the
-  // tile is then summed again with the reference at the tile maximum.
-  if (tv > -__builtin_inff()) rebase(pr, ref_for(tv));
-  if (!pr.cvalid) {
-    if (!have_max) {
-#pragma unroll
-      for (int j = 0; j < NE; ++j) lane_max = fmaxf(lane_max, x[j]);
-      have_max = true;
-    }
     const float m = wave_max_dpp(lane_max);
-    if (m > -__builtin_inff()) rebase(pr, ref_for(m));
+    if (m > -__builtin_inff()) rebase(pr, (int)uniform32((uint32_t)ref_for(m)));
   }
   if (pr.cvalid) {
     float sum = tile_exp_sum(x, pr.cref);
@@ -331,7 +305,7 @@ __device__ __forceinline__ void produce_tile(Producer& pr, TopkShared& sh, const
 #pragma unroll
         for (int j = 0; j < NE; ++j) lane_max = fmaxf(lane_max, x[j]);
       }
-      const int need = ref_for(wave_max_dpp(lane_max));
+      const int need = (int)uniform32((uint32_t)ref_for(wave_max_dpp(lane_max)));
       if (need > pr.cref) {
         pr.s = ldexpf(pr.s, pr.cref - need);
         pr.cref = need;
@@ -342,6 +316,64 @@ __device__ __forceinline__ void produce_tile(Producer& pr, TopkShared& sh, const
   }
 }
 
+// One full tile of U chunks per lane (chunk u of lane l holds elements tile_min_id + (u*64 + l)*EPC
+// onwards). Chunks whose maximum reaches the threshold value (exceeds it when the screen is strict)
+// are staged for the consumer, which tests their elements' full keys; then the exp sums.
+template <bool BF16>
+__device__ __forceinline__ void produce_tile(Producer& pr, TopkShared& sh,
+                                             const u32x4 (&raw)[kPerLane / ElemTraits<BF16>::kEPC],
+                                             uint32_t tile_min_id, uint32_t body_end_id, int K,
+                                             bool first) {
+  constexpr int EPC = ElemTraits<BF16>::kEPC;
+  constexpr int U = kPerLane / EPC;
+  const int lane = lane_id();
+  float x[kPerLane];
+  unpack_tile<BF16>(raw, x);
+  uint64_t T = producer_T(pr, sh);
+  if (first) {
+    float lane_max = -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) lane_max = fmaxf(lane_max, x[j]);
+    T = seed_from(pr, sh, T, lane_max, K);
+  }
+  T = uniform64(T);
+  const float tv = key_value(T);
+  // strict screen: x > value(T) (see strict_ok); on the integer bf16 patterns that is >= tb + 1.
+  // Everything here derives from the wave-uniform key T, so the branches are scalar.
+  const bool strict = strict_ok(T, tile_min_id);
+  const uint32_t thi = (uint32_t)(T >> 32);  // order bits of the threshold value
+  uint64_t mk[U];
+  if (BF16 && !first && thi > 0x80000000u) {
+    // positive threshold: its bf16 pattern is the high half of the fp32 bits (logits are bf16)
+    const int tbe = (int)(((thi & 0x7fffffffu) >> 16) + (strict ? 1u : 0u));
+#pragma unroll
+    for (int u = 0; u < U; ++u) mk[u] = __ballot(bf16_chunk_max(raw[u]) >= tbe);
+  } else {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float cm = x[u * EPC];
+#pragma unroll
+      for (int e = 1; e < EPC; ++e) cm = fmaxf(cm, x[u * EPC + e]);
+      mk[u] = strict ? __ballot(cm > tv) : __ballot(cm >= tv);
+    }
+  }
+  uint64_t anym = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) anym |= mk[u];
+  if (anym) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (!mk[u]) continue;
+      const uint32_t id0 = tile_min_id + (uint32_t)((u * kWave + lane) * EPC);
+      // elements past the segment end (the padded last tile) are masked out
+      const int nv = (int)min(max((int64_t)body_end_id - (int64_t)id0, (int64_t)0), (int64_t)EPC);
+      stage_chunks(pr, sh, raw[u], id0, (1u << nv) - 1u, (mk[u] >> lane) & 1u, mk[u]);
+    }
+    publish_tail(pr, sh);
+  }
+  exp_accumulate<kPerLane>(pr, x, T);
+}
+
 // ---- consumer ---------------------------------------------------------------------------------
 
 struct Consumer {
@@ -349,13 +381,10 @@ struct Consumer {
   uint64_t T_own;  // (u) key of the list's K-th entry, 0 while the list is not full
 };
 
-// Merge a batch of up to 64 keys (one per lane, 0 = none) into the list.
-__device__ __forceinline__ void consume_batch(Consumer& c, TopkShared& sh, uint64_t v, int K) {
+// Merge a batch of up to 64 keys (one per lane, 0 = none) that beat T into the list.
+__device__ __forceinline__ void consume_batch(Consumer& c, TopkShared& sh, uint64_t v, uint64_t T,
+                                              uint64_t m, int K) {
   const int lane = lane_id();
-  uint64_t T = atomic_load_T(sh);
-  if (c.T_own > T) T = c.T_own;
-  uint64_t m = __ballot(v > T);
-  if (!m) return;
   const uint64_t before = c.T_own;
   if (__popcll(m) > 8) {
     // many keys: bitonic sort of the batch, then a bitonic merge with the list
@@ -380,8 +409,44 @@ __device__ __forceinline__ void consume_batch(Consumer& c, TopkShared& sh, uint6
   if (c.T_own > before) publish_T(sh, c.T_own);
 }
 
+// Expand a batch of staged chunks (one per lane; mask 0 = none) into keys, element position by
+// element position, and merge those that beat the threshold. The threshold has usually risen
+// since the chunks were staged: a lane whose chunk maximum is below its value drops out first,
+// and an element position is skipped when no lane's element reaches that value.
+template <bool BF16>
+__device__ __forceinline__ void consume_chunks(Consumer& c, TopkShared& sh, const u32x4& r,
+                                               uint32_t id0, uint32_t mask, int K) {
+  constexpr int EPC = ElemTraits<BF16>::kEPC;
+  uint64_t T = atomic_load_T(sh);
+  if (c.T_own > T) T = c.T_own;
+  T = uniform64(T);
+  const uint32_t thi = (uint32_t)(T >> 32);
+  if (BF16 && thi > 0x80000000u) {
+    const int tb = (int)((thi & 0x7fffffffu) >> 16);
+    if (bf16_chunk_max(r) < tb) mask = 0u;
+  }
+  if (!__ballot(mask != 0u)) return;
+  const float tv = key_value(T);
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) {
+    const float v = chunk_elem<BF16>(r, e);
+    const bool q = ((mask >> e) & 1u) && v >= tv;
+    if (!__ballot(q)) continue;
+    const uint64_t key = q ? make_key(v, id0 + (uint32_t)e) : 0ull;
+    const uint64_t m = __ballot(key > T);
+    if (m) {
+      consume_batch(c, sh, key, T, m, K);
+      if (c.T_own > T) T = uniform64(c.T_own);
+    }
+  }
+}
+
+template <bool BF16>
 __device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K) {
   const int lane = lane_id();
+  // the consumer's batches are short and on the path of every producer's threshold: it takes
+  // issue priority over the producer waves it shares a SIMD with
+  __builtin_amdgcn_s_setprio(3);
   uint32_t head[kProducers];
 #pragma unroll
   for (int p = 0; p < kProducers; ++p) head[p] = 0;
@@ -392,11 +457,18 @@ __device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K) 
       const uint32_t t = uniform32(__hip_atomic_load(&sh.tail[p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
       while (head[p] != t) {
         const uint32_t n = t - head[p] < (uint32_t)kWave ? t - head[p] : (uint32_t)kWave;
-        const uint64_t v = (uint32_t)lane < n ? sh.ring[p][(head[p] + lane) & (kRing - 1)] : 0ull;
+        u32x4 r = u32x4{0u, 0u, 0u, 0u};
+        uint2 im = make_uint2(0u, 0u);
+        if ((uint32_t)lane < n) {
+          const StagedChunk& e = sh.ring[p][(head[p] + lane) & (kRing - 1)];
+          r = e.raw;
+          im = *reinterpret_cast<const uint2*>(&e.id0);
+        }
         head[p] += n;
+        // the release orders the reads above before the slots are handed back
         if (lane == 0)
           __hip_atomic_store(&sh.head[p], head[p], __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-        consume_batch(c, sh, v, K);
+        consume_chunks<BF16>(c, sh, r, im.x, im.y, K);
         any = true;
       }
     }
@@ -452,7 +524,7 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
   __shared__ TopkShared sh;
 
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = (int)uniform32(threadIdx.x / kWave);
   const int64_t row = blockIdx.x / split;
   const int part = blockIdx.x % split;
   const int64_t rowbase = row * V;
@@ -490,7 +562,7 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
   cons.L = 0;
   cons.T_own = 0;
   if (wave == 0) {
-    consume_all(cons, sh, K);
+    consume_all<BF16>(cons, sh, K);
   } else {
     Producer pr;
     pr.p = wave - 1;
@@ -504,23 +576,6 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
     // at a time); its tiles come in increasing id order
     const uint32_t body_end_id = (uint32_t)(c_end * EPC - rowbase);
     bool first = true;
-    auto process = [&](u32x4 (&raw)[U], int64_t t) {
-      if ((t + 1) * TILE > nchunks) pad_tile<BF16>(raw, t * TILE, nchunks);
-      float x[kPerLane];
-      unpack_tile<BF16>(raw, x);
-      const int64_t tc0 = c_beg + t * TILE;
-      const uint32_t tile_min_id = (uint32_t)(tc0 * EPC - rowbase);
-      // id of element j of this lane: the per-lane base is made opaque to the optimiser, which
-      // would otherwise keep all 32 (lane, j) offsets live across the loop
-      uint32_t lane_base = tile_min_id + (uint32_t)(lane * EPC);
-      __asm__ volatile("" : "+v"(lane_base));
-      auto id_of = [&](int j) -> uint32_t {
-        return lane_base + (uint32_t)((j / EPC) * kWave * EPC + (j % EPC));
-      };
-      auto valid_of = [&](int j) -> bool { return id_of(j) < body_end_id; };
-      produce_tile<kPerLane>(pr, sh, x, BF16 ? raw : nullptr, id_of, valid_of, K, first, tile_min_id);
-      first = false;
-    };
     // one tile in flight: the next tile's loads are issued (unconditionally: past the segment end
     // the bounded descriptor returns zeros without touching memory) before the current tile is
     // processed
@@ -531,24 +586,33 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
 #pragma unroll
       for (int u = 0; u < U; ++u) cur[u] = raw[u];
       load_tile<BF16>(raw, rsrc, (t + kProducers) * TILE);
-      process(cur, t);
+      if ((t + 1) * TILE > nchunks) pad_tile<BF16>(cur, t * TILE, nchunks);
+      const uint32_t tile_min_id = uniform32((uint32_t)((c_beg + t * TILE) * EPC - rowbase));
+      produce_tile<BF16>(pr, sh, cur, tile_min_id, body_end_id, K, first);
+      first = false;
     }
     if (wave == kTopkWaves - 1 && n_head + n_tail > 0) {
-      // ragged head/tail elements, one per lane
+      // ragged head/tail elements, one per lane, staged as one-element chunks without a screen
       float x1[1];
       int64_t g = -1;
       if (lane < n_head) g = g0 + lane;
       else if (lane < n_head + n_tail) g = c_end * EPC + (lane - n_head);
-      if (g >= 0) {
-        x1[0] = BF16 ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(logits)[g] << 16)
-                     : reinterpret_cast<const float*>(logits)[g];
-      } else {
-        x1[0] = -__builtin_inff();
+      uint32_t bits = BF16 ? 0xFF80u : 0xFF800000u;
+      if (g >= 0)
+        bits = BF16 ? (uint32_t)reinterpret_cast<const uint16_t*>(logits)[g]
+                    : reinterpret_cast<const uint32_t*>(logits)[g];
+      x1[0] = __uint_as_float(BF16 ? bits << 16 : bits);
+      uint64_t T = producer_T(pr, sh);
+      if (first) T = seed_from(pr, sh, T, x1[0], K);
+      const bool live = g >= 0;
+      const uint64_t m = __ballot(live);
+      if (m) {
+        const uint32_t pad = BF16 ? 0xFF80FF80u : 0xFF800000u;
+        const u32x4 r = u32x4{BF16 ? (bits | 0xFF800000u) : bits, pad, pad, pad};
+        stage_chunks(pr, sh, r, (uint32_t)(g - rowbase), 1u, live, m);
+        publish_tail(pr, sh);
       }
-      auto id_of1 = [&](int) -> uint32_t { return (uint32_t)(g - rowbase); };
-      auto valid_of1 = [&](int) -> bool { return g >= 0; };
-      // head ids precede the body: never screen strictly here
-      produce_tile<1>(pr, sh, x1, nullptr, id_of1, valid_of1, K, first, 0u);
+      exp_accumulate<1>(pr, x1, T);
     }
     const float ws = wave_sum(pr.s);
     if (lane == 0) {
