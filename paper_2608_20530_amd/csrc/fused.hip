@@ -5,8 +5,10 @@
 // leave the compute unit that made them.
 //
 // A workgroup owns up to P = 64 / K consecutive slot pairs (t, t+1) of one request:
-//  1. it gathers the embedding rows of the out side (slots t0 .. t0+P-1) and of the in side
-//     (slots t0+1 .. t0+P) into one bf16 LDS tile, 64 rows per side;
+//  1. it gathers the embedding rows of slots t0 .. t0+P once into one bf16 LDS tile: the out side
+//     (slots t0 .. t0+P-1) reads its 64 rows from the tile's start and the in side
+//     (slots t0+1 .. t0+P) from K rows further on, so the P-1 slots both sides share are
+//     gathered once;
 //  2. half of its waves project the out rows onto W_out and half the in rows onto W_in on the bf16
 //     matrix cores (exact three-term weight split), each wave owning four 16-column blocks;
 //  3. the raw projections u (fp32) replace the tile in LDS, with their squared norms;
@@ -154,7 +156,6 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   const int npair = anchor_wg ? 0 : (int)((B - 1 - t0) < plan.P ? (B - 1 - t0) : plan.P);
   const int n_out = npair * K;                 // out rows: slots t0 .. t0+npair-1
   const int n_in = anchor_wg ? K : npair * K;  // in rows: slots t0+1 .. (slot 0 for the anchor)
-  const int in_slot0 = anchor_wg ? 0 : t0 + 1;
   const int dpad = dkp * 32;
   const bool use_lp = lambda != 0.f;
   const float* lpn = logp + n * B * K;
@@ -168,25 +169,30 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
                             (size_t)cg * kNbPerWave * 1024 + lane * 16;
   BFrag b0;
   if (side_rows > 0) load_bfrag(b0, wf, slice, 0);  // in flight during the gather
-  for (int r = tid; r < 2 * kSideRows; r += nthreads) {
-    const int rs = r / kSideRows, lr = r % kSideRows;
+  // tile row r holds candidate r % K of slot s0 + r / K; the out side reads tile rows
+  // [0, 64), the in side tile rows [K, K + 64). Rows outside the workgroup's slots are zero (the
+  // anchor workgroup has only in rows, of slot 0: s0 = -1).
+  const int tile_rows = kSideRows + K;
+  const int s0 = anchor_wg ? -1 : t0;
+  const int s_lo = anchor_wg ? 0 : t0, s_hi = anchor_wg ? 0 : t0 + npair;
+  for (int r = tid; r < tile_rows; r += nthreads) {
+    const int slot = s0 + r / K;
     int32_t id = -1;
-    if (lr < (rs == 0 ? n_out : n_in)) {
-      const int slot = (rs == 0 ? t0 : in_slot0) + lr / K;
-      id = ids[(n * B + slot) * K + lr % K];
+    if (slot >= s_lo && slot <= s_hi) {
+      id = ids[(n * B + slot) * K + r % K];
       if (id < 0 || id >= V) id = -1;  // outside the table: a zero row
     }
     rid[r] = id;
   }
   __syncthreads();
-  gather_rows(A, plan.astride, 2 * kSideRows, rid, E, d, dpad, tid, nthreads);
+  gather_rows(A, plan.astride, tile_rows, rid, E, d, dpad, tid, nthreads);
   __syncthreads();
 
   // ---- 2. projection --------------------------------------------------------------------------
   f32x4 acc[kSideRm][kNbPerWave];
   if (side_rows > 0) {
-    project_tile<kSideRm>(acc, b0, A + lside * kSideRows * plan.astride, plan.astride, wf, slice,
-                          dkp, lane);
+    project_tile<kSideRm>(acc, b0, A + lside * K * plan.astride, plan.astride, wf, slice, dkp,
+                          lane);
     row_sumsq<kSideRm>(acc, ssw + (lside * plan.ws + cg) * kSideRows, lane);
   }
   __syncthreads();  // every wave is done reading the gathered tile
@@ -224,14 +230,28 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
       const bool ov = bl * 16 + r16 < K, iv = br * 16 + r16 < K;
       const float* po = Vf + orow * plan.vstride + 4 * q;
       const float* pi = Vf + irow * plan.vstride + 4 * q;
-      f32x4 c = f32x4{0.f, 0.f, 0.f, 0.f};
-      // MFMA step (s, e) contracts column 16 s + 4 q + e of both sides
-      for (int s = 0; s < d; s += 16) {
-        const f32x4 a = ov ? *reinterpret_cast<const f32x4*>(po + s) : f32x4{0.f, 0.f, 0.f, 0.f};
-        const f32x4 b = iv ? *reinterpret_cast<const f32x4*>(pi + s) : f32x4{0.f, 0.f, 0.f, 0.f};
+      // MFMA step (s, e) contracts column 16 s + 4 q + e of both sides, into one of four
+      // independent accumulators (one per e), so consecutive MFMAs never wait on each other
+      f32x4 ce[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
+      for (int e = 0; e < 4; ++e) ce[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // four steps per trip: their eight LDS reads are issued before the first MFMA
+      // (d is a multiple of 16; a partial trip reads zeros)
+      for (int s = 0; s < d; s += 64) {
+        f32x4 a[4], b[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bool in_d = s + 16 * u < d;
+          a[u] = ov && in_d ? *reinterpret_cast<const f32x4*>(po + s + 16 * u) : f32x4{0.f, 0.f, 0.f, 0.f};
+          b[u] = iv && in_d ? *reinterpret_cast<const f32x4*>(pi + s + 16 * u) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            ce[e] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][e], b[u][e], ce[e], 0, 0, 0);
       }
+      const f32x4 c = (ce[0] + ce[1]) + (ce[2] + ce[3]);
       // lane (r16, q) holds rows 4 q + i, column r16 of the tile
       const int kk = br * 16 + r16;
 #pragma unroll
@@ -320,13 +340,18 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   }
 
   // ---- 6. ticket; the request's last workgroup walks -----------------------------------------
-  // The workgroup barrier completes every wave's stores; one thread then releases them to the
-  // whole device and takes the ticket. Only the request's last workgroup acquires (a device-wide
-  // fence in every thread, or an acquire in every workgroup, would invalidate cached weights
-  // under the other workgroups still running: measured 2.7x slower).
+  // Everything the last workgroup reads (table rows, score blocks, contender masks) went out with
+  // device-coherent stores: once every wave has waited for its own stores to complete they are
+  // visible to the whole device, and one thread takes the ticket. The certified rule also
+  // releases with a device-wide fence, because its last workgroup overwrites pair scores that
+  // the others wrote with ordinary stores (a write-back of this compute unit's L2 orders them
+  // first). Only the request's last workgroup acquires (a device-wide fence in every thread, or
+  // an acquire in every workgroup, would invalidate cached weights under the other workgroups
+  // still running: measured 2.7x slower).
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (CERT) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     const uint32_t done =
         __hip_atomic_fetch_add(&counters[n], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *flag = done == (uint32_t)(plan.wg - 1);

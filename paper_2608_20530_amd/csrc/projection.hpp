@@ -105,11 +105,18 @@ __device__ __forceinline__ void project_tile(f32x4 (&acc)[RM][kNbPerWave], BFrag
 #pragma unroll
     for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   BFrag b1;
+  // the scheduling barriers keep each k-block's twelve fragment loads issued together ahead of
+  // the MFMAs of the previous one: left alone, the scheduler interleaves them into the MFMA
+  // stream to save registers and then waits on loads it has just issued
   for (int kb = 0; kb < dkp; kb += 2) {
     load_bfrag(b1, wf, slice, kb + 1);
+    __builtin_amdgcn_sched_barrier(0);
     mfma_kblock<RM>(acc, b0, A, astride, kb, lane);
+    __builtin_amdgcn_sched_barrier(0);
     load_bfrag(b0, wf, slice, kb + 2 < dkp ? kb + 2 : dkp - 1);
+    __builtin_amdgcn_sched_barrier(0);
     mfma_kblock<RM>(acc, b1, A, astride, kb + 1, lane);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
