@@ -108,6 +108,16 @@ constexpr float kBig = 0x1p64f;  // a tile sum above this is recomputed with a h
 template <int NE>
 __device__ __forceinline__ float tile_exp_sum(const float (&x)[NE], int cref) {
   const float c = -(float)cref;
+  if (NE >= 4) {
+    // the four partial sums start from the first four terms (no additions to zero)
+    float q[4];
+#pragma unroll
+    for (int j = 0; j < NE; ++j) {
+      const float e = __builtin_amdgcn_exp2f(fmaf(x[j], kLog2eF, c));
+      q[j & 3] = j < 4 ? e : q[j & 3] + e;
+    }
+    return (q[0] + q[1]) + (q[2] + q[3]);
+  }
   float q[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < NE; ++j) q[j & 3] += __builtin_amdgcn_exp2f(fmaf(x[j], kLog2eF, c));
@@ -130,12 +140,13 @@ __device__ __forceinline__ void load_tile(u32x4 (&raw)[kPerLane / ElemTraits<BF1
                                           __amdgpu_buffer_rsrc_t rsrc, int64_t rel_chunk0) {
   constexpr int U = kPerLane / ElemTraits<BF16>::kEPC;
   const int lane = lane_id();
+  // one lane offset; the chunk-block steps (1 KB apart) go into the instruction's offset field.
+  // Cache policy 3 (sc0 nt): streaming data, read once (measured fastest for this pass).
+  const uint32_t base = (uint32_t)(rel_chunk0 + lane) * 16u;
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const uint32_t off = (uint32_t)((rel_chunk0 + (int64_t)u * kWave + lane) * 16);
-    // cache policy 3 (sc0 nt): streaming data, read once (measured fastest for this pass)
-    raw[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 3));
-  }
+  for (int u = 0; u < U; ++u)
+    raw[u] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, base + (uint32_t)u * 1024u, 0, 3));
 }
 
 template <bool BF16>
@@ -203,6 +214,7 @@ struct Producer {
   int cref;         // (u) log2-units reference of the exp sums
   int cvalid;       // (u) cref is set
   float s;          // per-lane partial sum of exp2(x*log2e - cref)
+  uint64_t lastT;   // (u) threshold key the reference last followed
 };
 
 __device__ __forceinline__ void rebase(Producer& pr, int need) {
@@ -288,7 +300,10 @@ __device__ __forceinline__ uint64_t seed_from(Producer& pr, TopkShared& sh, uint
 template <int NE>
 __device__ __forceinline__ void exp_accumulate(Producer& pr, const float (&x)[NE], uint64_t T) {
   // T is wave-uniform: the reference is computed on the vector unit and read back as a scalar
-  if (T != 0) rebase(pr, (int)uniform32((uint32_t)ref_for(key_value(T))));
+  if (T != 0 && T != pr.lastT) {
+    rebase(pr, (int)uniform32((uint32_t)ref_for(key_value(T))));
+    pr.lastT = T;
+  }
   float lane_max = -__builtin_inff();
   bool have_max = false;
   if (!pr.cvalid) {
@@ -346,8 +361,29 @@ __device__ __forceinline__ void produce_tile(Producer& pr, TopkShared& sh,
   if (BF16 && !first && thi > 0x80000000u) {
     // positive threshold: its bf16 pattern is the high half of the fp32 bits (logits are bf16)
     const int tbe = (int)(((thi & 0x7fffffffu) >> 16) + (strict ? 1u : 0u));
+    // tile maximum first (one compare); the chunks are tested only when some lane passes
+    i16x2 cm2[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) mk[u] = __ballot(bf16_chunk_max(raw[u]) >= tbe);
+    for (int u = 0; u < U; ++u) {
+      const uint32_t w0 = raw[u][0], w1 = raw[u][1], w2 = raw[u][2], w3 = raw[u][3];
+      cm2[u] = __builtin_elementwise_max(
+          __builtin_elementwise_max(__builtin_bit_cast(i16x2, w0), __builtin_bit_cast(i16x2, w1)),
+          __builtin_elementwise_max(__builtin_bit_cast(i16x2, w2), __builtin_bit_cast(i16x2, w3)));
+    }
+    i16x2 tm = cm2[0];
+#pragma unroll
+    for (int u = 1; u < U; ++u) tm = __builtin_elementwise_max(tm, cm2[u]);
+    const int tmax = tm[0] > tm[1] ? (int)tm[0] : (int)tm[1];
+    if (__ballot(tmax >= tbe)) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int cm = cm2[u][0] > cm2[u][1] ? (int)cm2[u][0] : (int)cm2[u][1];
+        mk[u] = __ballot(cm >= tbe);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u) mk[u] = 0;
+    }
   } else {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -572,6 +608,7 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
     pr.cref = 0;
     pr.cvalid = 0;
     pr.s = 0.f;
+    pr.lastT = 0;
     // producer p streams tiles p, p + 3, p + 6, ... (the workgroup reads one contiguous window
     // at a time); its tiles come in increasing id order
     const uint32_t body_end_id = (uint32_t)(c_end * EPC - rowbase);
