@@ -615,18 +615,21 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
     bool first = true;
     // one tile in flight: the next tile's loads are issued (unconditionally: past the segment end
     // the bounded descriptor returns zeros without touching memory) before the current tile is
-    // processed
-    u32x4 raw[U];
-    load_tile<BF16>(raw, rsrc, (int64_t)pr.p * TILE);
-    for (int64_t t = pr.p; t < ntiles; t += kProducers) {
-      u32x4 cur[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) cur[u] = raw[u];
-      load_tile<BF16>(raw, rsrc, (t + kProducers) * TILE);
+    // processed. Two register buffers alternate (the loop is unrolled by two), so a tile is
+    // processed in the registers it was loaded into rather than copied out of them.
+    auto step = [&](u32x4 (&cur)[U], u32x4 (&nxt)[U], int64_t t) {
+      load_tile<BF16>(nxt, rsrc, (t + kProducers) * TILE);
       if ((t + 1) * TILE > nchunks) pad_tile<BF16>(cur, t * TILE, nchunks);
       const uint32_t tile_min_id = uniform32((uint32_t)((c_beg + t * TILE) * EPC - rowbase));
       produce_tile<BF16>(pr, sh, cur, tile_min_id, body_end_id, K, first);
       first = false;
+    };
+    u32x4 ra[U], rb[U];
+    load_tile<BF16>(ra, rsrc, (int64_t)pr.p * TILE);
+    for (int64_t t = pr.p; t < ntiles; t += 2 * kProducers) {
+      step(ra, rb, t);
+      if (t + kProducers >= ntiles) break;
+      step(rb, ra, t + kProducers);
     }
     if (wave == kTopkWaves - 1 && n_head + n_tail > 0) {
       // ragged head/tail elements, one per lane, staged as one-element chunks without a screen
