@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--no-stress", action="store_true", help="skip the stress logits-pass line")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload line (both metrics at every workload)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
     return ap.parse_args()
@@ -89,10 +91,10 @@ def time_logits_pass(L, torch, cfg, logits_list, iters, warmup):
     return statistics.mean(t), statistics.median(t), q(0.1), q(0.9)
 
 
-def stream_read_rate(torch, bufs, iters=20, warmup=3):
-    """GB/s of a plain streaming read (16-byte streaming-policy buffer loads, the logits pass's own
-    load path, one contiguous segment per workgroup) over the same resident buffers, rotated like
-    the logits pass reads them: the read ceiling the logits pass is compared with."""
+def stream_reader(torch):
+    """A launcher of the plain streaming read (16-byte streaming-policy buffer loads, the logits
+    pass's own load path, one contiguous segment per workgroup) of one resident buffer, queued on
+    the current stream."""
     import ctypes
 
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_20530_amd", "libbench_read.so"))
@@ -101,14 +103,20 @@ def stream_read_rate(torch, bufs, iters=20, warmup=3):
     lib.bench_stream_read.restype = ctypes.c_int
     grid = 1024
     sink = torch.empty(grid * 256, dtype=torch.int32, device="cuda")
-    stream = torch.cuda.current_stream().cuda_stream
 
-    def run(i):
-        b = bufs[i % len(bufs)]
+    def read(b):
         rc = lib.bench_stream_read(b.data_ptr(), b.numel() * b.element_size(), sink.data_ptr(),
-                                   grid, stream)
+                                   grid, torch.cuda.current_stream().cuda_stream)
         if rc != 0:
             raise RuntimeError(f"bench_stream_read failed ({rc})")
+    return read
+
+
+def stream_read_rate(torch, bufs, iters=20, warmup=3):
+    """GB/s of the plain streaming read over the same resident buffers, rotated like the logits
+    pass reads them: the read ceiling the logits pass is compared with."""
+    read = stream_reader(torch)
+    run = lambda i: read(bufs[i % len(bufs)])
 
     for i in range(warmup):
         run(i)
@@ -138,6 +146,74 @@ def median_launch_us(torch, fn, iters=50, warmup=5):
         b.record()
     torch.cuda.synchronize()
     return statistics.median(a.elapsed_time(b) for a, b in ev) * 1e3
+
+
+def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
+    """Both metrics at one workload: blocks/s of the step (logits pass, then the fused pass or the
+    separate calls) and the logits pass's GB/s, each the mean over `iters` back-to-back calls
+    between two HIP events. The logits rotate over enough resident copies (at least 1 GiB in all)
+    that every call reads its logits from HBM, as in the headline loop."""
+    lg = inp["logits"].cuda()
+    nbytes = lg.numel() * lg.element_size()
+    copies = max(1, min(1024, -(-(1 << 30) // nbytes)))
+    lgs = [lg] + [lg.clone() for _ in range(copies - 1)]
+    E = inp["E"].cuda()
+    packed = L.pack_weights(inp["W_in"].cuda(), inp["W_out"].cuda())
+    N, B, K, V = c.N, c.B, c.K, c.V
+    ids = torch.empty(N, B, K, dtype=torch.int32, device="cuda")
+    logp = torch.empty(N, B, K, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(L.lilicorr_topk_workspace_bytes(N, B, V, K), 16), dtype=torch.uint8,
+                     device="cuda")
+    draft = torch.empty(N, B, dtype=torch.int32, device="cuda")
+    choice = torch.empty_like(draft)
+    logq = torch.empty(N, B, dtype=torch.float32, device="cuda")
+    # the fused pass holds both sides' fp32 projections in LDS (bf16 tables, d <= 256); other
+    # workloads take the separate calls
+    fused = E.dtype == torch.bfloat16 and c.d <= 256
+    if fused:
+        ws_fused = L.score_walk_workspace(N, B, K)
+
+        def rest():
+            L.score_walk(ids, logp, E, packed, None, L.SIGMA, 0.0, out=(draft, choice, logq),
+                         workspace=ws_fused)
+    else:
+        in_vec = torch.empty(N, B, K, c.d, dtype=torch.float32, device="cuda")
+        out_vec = torch.empty_like(in_vec)
+        S = torch.empty(N, max(B - 1, 1), K, K, dtype=torch.float32, device="cuda")
+
+        def rest():
+            L.candidate_vectors(ids, E, packed, out=(in_vec, out_vec))
+            L.pair_scores(in_vec, out_vec, None, L.SIGMA, out=(S, None))
+            L.greedy_walk(S, None, logp, ids, 0.0, out=(draft, choice, logq))
+
+    topk = lambda i: L.topk(lgs[i % copies], K, out=(ids, logp), workspace=ws)
+    counter = [0]
+
+    def batch(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(iters):
+            fn(counter[0])
+            counter[0] += 1
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / 1e3 / iters
+
+    for _ in range(warmup):
+        topk(counter[0])
+        rest()
+        counter[0] += 1
+    step = batch(lambda i: (topk(i), rest()))
+    t_topk = batch(topk)
+    return {"workload": f"{c.name}: N={N}, B={B}, K={K}, V={V}, d={c.d}, "
+                        f"{'bf16' if lg.element_size() == 2 else 'fp32'} logits",
+            "path": "lilicorr_topk -> " + ("lilicorr_score_walk" if fused else
+                                            "candidate_vectors -> pair_scores -> greedy_walk"),
+            "logits_copies": copies,
+            "blocks_s": N / step, "step_us": step * 1e6,
+            "logits_GB_s": nbytes / t_topk / 1e9, "logits_us": t_topk * 1e6,
+            "logits_frac_of_8TBs": nbytes / t_topk / 1e9 / PEAK_HBM_GBS}
 
 
 def cpu_baseline(cfg, inp, seconds):
@@ -333,7 +409,7 @@ def main():
         plain_us = median_launch_us(torch, lambda: L.topk(logits_list[0], K, out=(ids, logp),
                                                           workspace=ws))
         read3 = stream_read_rate(torch, logits_list)
-        del logits_list
+        logits_list = None
         torch.cuda.empty_cache()
         t4, m4, lo4, hi4 = time_logits_pass(L, torch, c4, [lg4], iters=20, warmup=3)
         read4 = stream_read_rate(torch, [lg4])
@@ -351,6 +427,21 @@ def main():
                        "workload": "N=256, B=16, K=32, V=262144, bf16 logits"},
         }
         del lg4
+
+    if not args.no_configs:
+        # both metrics at every workload (the headline's figures here come from the cold-step
+        # protocol of per_config_rates, not from the timed loop above)
+        logits_list = None
+        torch.cuda.empty_cache()
+        per = {}
+        for ci in range(len(workloads.CONFIGS)):
+            c = workloads.config(ci)
+            pinp = inp if ci == cfg.index else workloads.make_inputs(c)
+            per[c.name] = per_config_rates(L, torch, c, pinp)
+            del pinp
+            torch.cuda.empty_cache()
+            print(f"[bench] workload {c.name} done", file=sys.stderr, flush=True)
+        out["per_workload"] = per
 
     if args.calibrate_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
