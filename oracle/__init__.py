@@ -6,6 +6,7 @@ CPU-baseline leg; the product path never imports it. It shares no code with the 
 All arrays are numpy, C-contiguous, on the host. bf16 tensors are passed as their uint16 bit
 patterns. Each function mirrors one call of the library and returns fresh output arrays.
 Parity status of every function is pinned by tests/test_oracle_*.py (see the design notes).
+The scoring-Transformer stand-in's oracle is the numpy module `oracle.scorer`.
 """
 from __future__ import annotations
 

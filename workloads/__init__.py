@@ -29,6 +29,14 @@ Recipe per config (index: shapes; logits; vectors):
 4: N=256, B=16, K=32, V=262144, d=512. bf16 N(0,3^2); +8 at one uniform id in each slot of a
    Bernoulli(1/2) subset of slots. E [V,512] bf16 N(0,0.02^2); W [512,512] fp32 N(0,1/512).
 
+Scoring-Transformer stand-in (a cost-only stand-in of the head's encoder: random weights, no
+trained values exist here). ScorerConfig: N requests, S slots, K candidates (L = S*K nodes),
+width H, heads, feed-forward width F, layers. Node states X [N][L][H] fp32 N(0,1); per layer:
+w_qkv [H][3H], w_o [H][H], w_1 [H][F] bf16 N(0, 1/H), w_2 [F][H] bf16 N(0, 1/F); RMSNorm gains
+g_attn, g_ffn [H] fp32 1 + 0.1 N(0,1); attention biases dist_bias [heads][2S-1] and
+same_bias [heads] fp32 0.5 N(0,1). The headline shape is N=64, S=15 (16-slot blocks, 15 drafted),
+K=16, H=1024, 8 heads, F=2048, 2 layers (the paper's head widths and depth).
+
 Measured softmax entropy over V=151936 without bumps: std 0.5 -> 11.8 nats (high-entropy
 tier), std 2 -> 9.9 nats (mid), std 4 -> 5.0 nats (low).
 """
@@ -40,7 +48,8 @@ from dataclasses import dataclass
 import torch
 
 __all__ = ["Config", "CONFIGS", "config", "make_logits", "make_request_logits",
-           "make_embedding", "make_weights", "make_inputs", "make_anchor"]
+           "make_embedding", "make_weights", "make_inputs", "make_anchor", "ScorerConfig",
+           "SCORER_HEADLINE", "make_scorer_inputs"]
 
 
 @dataclass(frozen=True)
@@ -165,3 +174,43 @@ def make_anchor(cfg: Config) -> torch.Tensor:
 def make_inputs(cfg: Config) -> dict:
     w_in, w_out = make_weights(cfg)
     return {"logits": make_logits(cfg), "E": make_embedding(cfg), "W_in": w_in, "W_out": w_out}
+
+
+@dataclass(frozen=True)
+class ScorerConfig:
+    N: int
+    S: int
+    K: int
+    H: int = 1024
+    heads: int = 8
+    F: int = 2048
+    layers: int = 2
+    seed: int = 7
+
+    @property
+    def L(self) -> int:
+        return self.S * self.K
+
+
+SCORER_HEADLINE = ScorerConfig(N=64, S=15, K=16)
+
+_TAG_SX, _TAG_SW = 11, 12
+
+
+def make_scorer_inputs(sc: ScorerConfig) -> dict:
+    """{"X": [N][L][H] fp32, "layers": [dict of CPU tensors per layer]} (see the module notes)."""
+    H, F, S, heads = sc.H, sc.F, sc.S, sc.heads
+    X = torch.randn(sc.N, sc.L, H, generator=_gen(sc.seed, _TAG_SX), dtype=torch.float32)
+    layers = []
+    for i in range(sc.layers):
+        g = _gen(sc.seed, _TAG_SW, i)
+        w = lambda r, c, fan: (torch.randn(r, c, generator=g) / math.sqrt(fan)).to(torch.bfloat16)
+        layers.append({
+            "w_qkv": w(H, 3 * H, H).contiguous(), "w_o": w(H, H, H).contiguous(),
+            "w_1": w(H, F, H).contiguous(), "w_2": w(F, H, F).contiguous(),
+            "g_attn": (1 + 0.1 * torch.randn(H, generator=g)).contiguous(),
+            "g_ffn": (1 + 0.1 * torch.randn(H, generator=g)).contiguous(),
+            "dist_bias": (0.5 * torch.randn(heads, 2 * S - 1, generator=g)).contiguous(),
+            "same_bias": (0.5 * torch.randn(heads, generator=g)).contiguous(),
+        })
+    return {"X": X.contiguous(), "layers": layers}
