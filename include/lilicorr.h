@@ -300,6 +300,60 @@ lilicorr_status lilicorr_block_graph_launch(lilicorr_graph *graph, hipStream_t s
 /* Releases the graph (NULL is ignored); the caller makes sure no replay is still running. */
 void lilicorr_block_graph_destroy(lilicorr_graph *graph);
 
+/*
+ * Scoring-Transformer stand-in — the encoder of the paper's speculative head (implementation
+ * appendix, "Architecture"; widths and depth from the hyper-parameter table): a stack of
+ * bidirectional Transformer layers over each request's candidate lattice of S slots x K
+ * candidates (L = S * K nodes, node j in slot j / K), width H, H / 128 heads of width 128,
+ * feed-forward width F, RMSNorm and SiLU, with two learned per-head attention biases added to the
+ * attention logits: one indexed by the signed slot distance (query slot - key slot), one added
+ * when both nodes share a slot. Each layer is pre-norm:
+ *     x += Wo . attn(rmsnorm(x; g_attn));   x += W2 . silu(W1 . rmsnorm(x; g_ffn))
+ * with rmsnorm(x; g) = x / sqrt(mean(x^2) + 1e-6) * g, attention logits scaled by 1/sqrt(128),
+ * every node attending to every node of its request. A cost-only stand-in: the weights are the
+ * caller's (random here); there is no trained head. Precision: bf16 weights; every matrix-core
+ * input (normalised activations, Q, K, V, attention probabilities, attention output, SiLU output)
+ * is rounded to bf16 (nearest, ties to even); fp32 accumulation; fp32 residual stream.
+ *
+ * One layer's parameters, all device pointers (weights as raw bf16 bit patterns, applied as
+ * y = x W):
+ *   w_qkv     [H][3H]  columns [0,H) = Q, [H,2H) = K, [2H,3H) = V; head h owns columns
+ *                      h*128 .. h*128+127 of each part
+ *   w_o       [H][H];  w_1 [H][F];  w_2 [F][H]
+ *   g_attn, g_ffn  [H] fp32 RMSNorm gains
+ *   dist_bias [heads][2S-1] fp32: entry (S-1) + (s_query - s_key)
+ *   same_bias [heads] fp32
+ */
+typedef struct {
+    const uint16_t *w_qkv, *w_o, *w_1, *w_2;
+    const float *g_attn, *g_ffn, *dist_bias, *same_bias;
+} lilicorr_scorer_layer;
+
+/* Bytes of one packed layer (weights transposed for the matrix cores, gains, biases) for these
+ * sizes; 0 if the sizes are unsupported. */
+size_t lilicorr_scorer_packed_bytes(int H, int heads, int F, int64_t S);
+
+/* Packs one layer into `packed` (device, 16-byte aligned, lilicorr_scorer_packed_bytes bytes,
+ * caller-owned). `layer` is a host struct of device pointers, read on the stream; the packed
+ * layer serves every forward call with the same H, heads, F and S.
+ * Limits: H a multiple of 256 with 256 <= H <= 4096 and heads = H / 128; F a multiple of 128
+ * with 128 <= F <= 16384; 1 <= S <= 256. */
+lilicorr_status lilicorr_scorer_pack(const lilicorr_scorer_layer *layer, int H, int heads, int F,
+                                     int64_t S, void *packed, hipStream_t stream);
+
+/* Device scratch bytes lilicorr_scorer_forward needs; 0 if the sizes are unsupported. */
+size_t lilicorr_scorer_workspace_bytes(int64_t N, int64_t S, int K, int H, int F);
+
+/* Runs `layers` packed layers over X [N][S*K][H] fp32 in place (device, 16-byte aligned).
+ * `packed` holds the layers back to back (layers * lilicorr_scorer_packed_bytes bytes, packed
+ * with the same H, heads, F and S). workspace: lilicorr_scorer_workspace_bytes bytes of device
+ * scratch, caller-owned, no initial contents needed, clobbered.
+ * Limits: those of lilicorr_scorer_pack, and 1 <= K, L = S*K <= 256, N >= 1,
+ * N*L*max(3H, F)*4 < 2^31. */
+lilicorr_status lilicorr_scorer_forward(float *X, int64_t N, int64_t S, int K, int H, int heads,
+                                        int F, int layers, const void *packed, void *workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char *lilicorr_status_string(lilicorr_status s);
 

@@ -13,6 +13,7 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
   lilicorr_score_walk_certified  the same pass, near-tied decisions decided again in fp64
   lilicorr_score_viterbi      the same pass with the exact max-path decode
   lilicorr_block_graph_*      top-K + one fused pass recorded as one HIP graph, replayed per block
+  lilicorr_scorer_*           scoring-Transformer stand-in over the candidate lattice (cost only)
 
 This module only marshals arguments: torch supplies device memory and the current HIP stream,
 and every step of the path runs in the library's kernels. There is no fallback: if the library
@@ -36,6 +37,9 @@ __all__ = [
     "BlockArgs", "BlockGraph", "lilicorr_status_string",
     "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk", "score_viterbi",
     "score_walk_certified", "score_walk_certified_workspace", "CERT_MARGIN", "draft_block",
+    "ScorerLayer", "lilicorr_scorer_packed_bytes", "lilicorr_scorer_pack",
+    "lilicorr_scorer_workspace_bytes", "lilicorr_scorer_forward", "scorer_pack", "scorer_workspace",
+    "scorer_forward",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblilicorr.so")
@@ -72,6 +76,12 @@ class BlockArgs(ctypes.Structure):
     ]
 
 
+class ScorerLayer(ctypes.Structure):
+    """lilicorr_scorer_layer of include/lilicorr.h, field for field (device pointers)."""
+    _fields_ = [(name, ctypes.c_void_p) for name in
+                ("w_qkv", "w_o", "w_1", "w_2", "g_attn", "g_ffn", "dist_bias", "same_bias")]
+
+
 def load_library() -> ctypes.CDLL:
     global _lib
     if _lib is not None:
@@ -104,6 +114,10 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_block_graph_create": ([ctypes.POINTER(BlockArgs), ctypes.POINTER(P)], I),
         "lilicorr_block_graph_launch": ([P, P], I),
         "lilicorr_block_graph_destroy": ([P], None),
+        "lilicorr_scorer_packed_bytes": ([I, I, I, I64], SZ),
+        "lilicorr_scorer_pack": ([ctypes.POINTER(ScorerLayer), I, I, I, I64, P, P], I),
+        "lilicorr_scorer_workspace_bytes": ([I64, I64, I, I, I], SZ),
+        "lilicorr_scorer_forward": ([P, I64, I64, I, I, I, I, I, P, P, SZ, P], I),
         "lilicorr_status_string": ([I], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -563,3 +577,66 @@ def draft_block(logits: torch.Tensor, K: int, E: torch.Tensor, packed: torch.Ten
     draft, choice, logq = greedy_walk(S, S0, logp, ids, logp_weight)
     return {"ids": ids, "logp": logp, "in_vec": in_vec, "out_vec": out_vec, "S": S, "S0": S0,
             "draft": draft, "choice": choice, "logq": logq}
+
+
+# ---- scoring-Transformer stand-in ---------------------------------------------------------------
+
+def lilicorr_scorer_packed_bytes(H: int, heads: int, F: int, S: int) -> int:
+    return load_library().lilicorr_scorer_packed_bytes(H, heads, F, S)
+
+
+def lilicorr_scorer_pack(layer: ScorerLayer, H, heads, F, S, packed, stream) -> int:
+    return _call("lilicorr_scorer_pack", ctypes.byref(layer), H, heads, F, S, packed, stream)
+
+
+def lilicorr_scorer_workspace_bytes(N: int, S: int, K: int, H: int, F: int) -> int:
+    return load_library().lilicorr_scorer_workspace_bytes(N, S, K, H, F)
+
+
+def lilicorr_scorer_forward(X, N, S, K, H, heads, F, layers, packed, workspace, workspace_bytes,
+                            stream) -> int:
+    return _call("lilicorr_scorer_forward", X, N, S, K, H, heads, F, layers, packed, workspace,
+                 workspace_bytes, stream)
+
+
+def scorer_pack(layers: list, S: int) -> torch.Tensor:
+    """Packs the layers (dicts of device tensors: w_qkv [H,3H], w_o [H,H], w_1 [H,F], w_2 [F,H]
+    bf16; g_attn, g_ffn [H], dist_bias [heads, 2S-1], same_bias [heads] fp32) back to back."""
+    H = layers[0]["w_qkv"].shape[0]
+    F = layers[0]["w_1"].shape[1]
+    heads = layers[0]["same_bias"].shape[0]
+    nb = lilicorr_scorer_packed_bytes(H, heads, F, S)
+    if nb == 0:
+        raise LilicorrError(f"scorer does not support H={H}, heads={heads}, F={F}, S={S}")
+    out = torch.empty(len(layers) * nb, dtype=torch.uint8, device=layers[0]["w_qkv"].device)
+    shapes = {"w_qkv": (H, 3 * H), "w_o": (H, H), "w_1": (H, F), "w_2": (F, H), "g_attn": (H,),
+              "g_ffn": (H,), "dist_bias": (heads, 2 * S - 1), "same_bias": (heads,)}
+    for i, l in enumerate(layers):
+        ptrs = {}
+        for name, shape in shapes.items():
+            t = l[name]
+            if tuple(t.shape) != shape:
+                raise LilicorrError(f"layer {i} {name} has shape {tuple(t.shape)}, expected {shape}")
+            want = (torch.bfloat16,) if name.startswith("w_") else (torch.float32,)
+            ptrs[name] = _dev(t, name, want)
+        lilicorr_scorer_pack(ScorerLayer(**ptrs), H, heads, F, S, out.data_ptr() + i * nb, _stream())
+    return out
+
+
+def scorer_workspace(N: int, S: int, K: int, H: int, F: int, device="cuda") -> torch.Tensor:
+    need = lilicorr_scorer_workspace_bytes(N, S, K, H, F)
+    if need == 0:
+        raise LilicorrError(f"scorer does not support N={N}, S={S}, K={K}, H={H}, F={F}")
+    return torch.empty(need, dtype=torch.uint8, device=device)
+
+
+def scorer_forward(X: torch.Tensor, packed: torch.Tensor, S: int, K: int, heads: int, F: int,
+                   layers: int, *, workspace=None) -> torch.Tensor:
+    """Runs the packed layers over X [N, S*K, H] fp32 in place; returns X."""
+    N, L, H = X.shape
+    if L != S * K:
+        raise LilicorrError(f"X has {L} nodes per request, expected S*K = {S * K}")
+    ws = workspace if workspace is not None else scorer_workspace(N, S, K, H, F, X.device)
+    lilicorr_scorer_forward(_dev(X, "X", (torch.float32,)), N, S, K, H, heads, F, layers,
+                            _dev(packed, "packed"), _dev(ws, "workspace"), ws.numel(), _stream())
+    return X

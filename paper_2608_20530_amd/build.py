@@ -12,7 +12,7 @@ LIB = os.path.join(HERE, "liblilicorr.so")
 # measurement aid for bench.py (a plain streaming read), kept out of the path's library
 BENCH_LIB = os.path.join(HERE, "libbench_read.so")
 SOURCES = ["topk.hip", "vectors.hip", "pairs.hip", "walk.hip", "viterbi.hip", "fused.hip",
-           "graph.hip", "status.hip"]
+           "graph.hip", "scorer.hip", "status.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -277,3 +277,25 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(L.LilicorrError):
         L.load_library()
+
+
+def test_scorer_size_queries_and_rejections(L):
+    H, F, heads, S = 1024, 2048, 8, 15
+    packed = L.lilicorr_scorer_packed_bytes(H, heads, F, S)
+    # transposed weights (3H^2 + H^2 + 2 H F bf16) + gains + biases, each section 256-byte aligned
+    assert packed >= 2 * (4 * H * H + 2 * H * F) + 8 * H + 4 * heads * 2 * S
+    assert packed % 256 == 0
+    assert L.lilicorr_scorer_packed_bytes(320, 2, F, S) == 0      # H not a multiple of 256
+    assert L.lilicorr_scorer_packed_bytes(H, 4, F, S) == 0        # heads * 128 != H
+    assert L.lilicorr_scorer_packed_bytes(H, heads, 200, S) == 0  # F not a multiple of 128
+    assert L.lilicorr_scorer_packed_bytes(H, heads, F, 0) == 0
+    ws = L.lilicorr_scorer_workspace_bytes(64, 15, 16, H, F)
+    M = 64 * 240
+    assert ws >= 2 * (M * H + M * 2 * H + 64 * H * 240 + M * H + M * F)
+    assert L.lilicorr_scorer_workspace_bytes(1, 17, 16, H, F) == 0   # L = 272 > 256
+    assert L.lilicorr_scorer_workspace_bytes(0, 15, 16, H, F) == 0
+    # null pointers are rejected before anything is launched
+    assert L.load_library().lilicorr_scorer_forward(None, 1, 15, 16, H, heads, F, 2, None, None, 0,
+                                                    None) == -1
+    assert L.load_library().lilicorr_scorer_pack(ctypes.byref(L.ScorerLayer()), H, heads, F, S,
+                                                 None, None) == -1
