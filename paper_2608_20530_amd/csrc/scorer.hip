@@ -44,8 +44,9 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kHd = 128;  // head width
 constexpr float kEps = 1e-6f;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kBK = 64;
 constexpr int kGemmThreads = 256;
+constexpr int kGroup = 8;  // row blocks per tile group (L2 blocking of the GEMM grid)
 constexpr int kAttnThreads = 512;
 constexpr int kMaxL = 256;
 constexpr int kMaxH = 4096;
@@ -55,13 +56,16 @@ constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-__device__ __forceinline__ uint32_t bf16_rne(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even: one v_cvt_pk_bf16_f32 per pair of values on gfx950
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{lo, hi}), bf16x2));
 }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return bf16_rne(lo) | (bf16_rne(hi) << 16);
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+  return __builtin_bit_cast(uint16_t, (__bf16)x);
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
@@ -112,106 +116,168 @@ struct GemmArgs {
   int H, L, Lv;
 };
 
-template <int MODE>
+// One workgroup of four waves (2 x 2) computes a (32 WTM) x (32 WTN) tile; each wave a
+// (16 WTM) x (16 WTN) block of WTM x WTN accumulator tiles.
+template <int MODE, int WTM, int WTN>
 __global__ __launch_bounds__(kGemmThreads) void gemm_bf16_kernel(GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][kBM * kBK];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][kBN * kBK];
+  constexpr int BM = 32 * WTM, BN = 32 * WTN;
+  constexpr int CA = BM * 8 / kGemmThreads, CB = BN * 8 / kGemmThreads;  // chunks per thread
+  extern __shared__ __attribute__((aligned(16))) unsigned char gemm_smem[];
+  uint16_t* sA = reinterpret_cast<uint16_t*>(gemm_smem);   // [2][BM * kBK]
+  uint16_t* sB = sA + 2 * BM * kBK;                        // [2][BN * kBK]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int ntn = p.N / kBN;
-  const int64_t tm = blockIdx.x / ntn;
-  const int tn = (int)(blockIdx.x - tm * ntn);
-  const int64_t m0 = tm * kBM;
-  const int n0 = tn * kBN;
+  const int ntn = p.N / BN;
+  // Workgroups are dealt to the eight XCDs round robin; when the grid divides evenly, each XCD
+  // takes a contiguous run of tile numbers. Tile numbers run over groups of kGroup row blocks,
+  // column blocks outer, so the workgroups an XCD holds at once share A rows and B columns in
+  // its L2.
+  const uint32_t nt = gridDim.x;
+  const uint32_t t = (nt % 8u == 0u) ? (blockIdx.x % 8u) * (nt / 8u) + blockIdx.x / 8u
+                                     : blockIdx.x;
+  const int64_t ntm = (p.M + BM - 1) / BM;
+  const int64_t per_group = (int64_t)kGroup * ntn;
+  const int64_t grp = t / per_group;
+  const int64_t rows_in = (ntm - grp * kGroup) < kGroup ? (ntm - grp * kGroup) : kGroup;
+  const int64_t r = t - grp * per_group;
+  const int64_t tm = grp * kGroup + r % rows_in;
+  const int tn = (int)(r / rows_in);
+  const int64_t m0 = tm * BM;
+  const int n0 = tn * BN;
   const uint32_t K2 = (uint32_t)p.K * 2u;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, (uint32_t)p.M * K2);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.Bt, (uint32_t)p.N * K2);
 
-  // staging: each thread moves chunks tid + 256 j (j = 0..3) of both 128 x 64 tiles; chunk c is
-  // row c / 8, 16-byte column c % 8, stored at column (c % 8) ^ (row % 8)
-  uint32_t offA[4], offB[4];
-  int lds[4];
+  // staging: thread tid moves chunks tid + 256 j of each tile; chunk c is row c / 8, 16-byte
+  // column c % 8, stored at column (c % 8) ^ (row % 8)
+  uint32_t offA[CA], offB[CB];
+  int ldsA[CA], ldsB[CB];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < CA; ++j) {
     const int c = tid + j * kGemmThreads;
     const int row = c >> 3, kc = c & 7;
     offA[j] = (uint32_t)(m0 + row) * K2 + (uint32_t)kc * 16u;
-    offB[j] = (uint32_t)(n0 + row) * K2 + (uint32_t)kc * 16u;
-    lds[j] = row * kBK + ((kc ^ (row & 7)) << 3);
+    ldsA[j] = row * kBK + ((kc ^ (row & 7)) << 3);
   }
-  u32x4 ga[4], gb[4];
-  auto gload = [&](int k0) {
+#pragma unroll
+  for (int j = 0; j < CB; ++j) {
+    const int c = tid + j * kGemmThreads;
+    const int row = c >> 3, kc = c & 7;
+    offB[j] = (uint32_t)(n0 + row) * K2 + (uint32_t)kc * 16u;
+    ldsB[j] = row * kBK + ((kc ^ (row & 7)) << 3);
+  }
+  // two register sets: the loads of stage s + 2 are issued while stage s is multiplied, and
+  // stored to LDS only at the end of stage s + 1
+  u32x4 g0[CA + CB], g1[WTM * WTN > 16 ? 1 : CA + CB];
+  auto gload = [&](u32x4 (&g)[CA + CB], int k0) {
     const uint32_t kb = (uint32_t)k0 * 2u;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      ga[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, offA[j] + kb, 0, 0));
-      gb[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rb, offB[j] + kb, 0, 0));
-    }
-  };
-  auto lstore = [&](int buf) {
+    for (int j = 0; j < CA; ++j)
+      g[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, offA[j] + kb, 0, 0));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      *reinterpret_cast<u32x4*>(&sA[buf][lds[j]]) = ga[j];
-      *reinterpret_cast<u32x4*>(&sB[buf][lds[j]]) = gb[j];
-    }
+    for (int j = 0; j < CB; ++j)
+      g[CA + j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rb, offB[j] + kb, 0, 0));
+  };
+  auto lstore = [&](const u32x4 (&g)[CA + CB], int buf) {
+#pragma unroll
+    for (int j = 0; j < CA; ++j) *reinterpret_cast<u32x4*>(&sA[buf * BM * kBK + ldsA[j]]) = g[j];
+#pragma unroll
+    for (int j = 0; j < CB; ++j) *reinterpret_cast<u32x4*>(&sB[buf * BN * kBK + ldsB[j]]) = g[CA + j];
   };
 
   // fragment reads: row (lane & 15) of each 16-row block, k chunk ks * 4 + lane / 16
-  int rowA[4], rowB[4], sw[2];
+  int rowA[WTM], rowB[WTN], sw[2];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    rowA[t] = (wm * 64 + t * 16 + (lane & 15)) * kBK;
-    rowB[t] = (wn * 64 + t * 16 + (lane & 15)) * kBK;
-  }
+  for (int i = 0; i < WTM; ++i) rowA[i] = (wm * 16 * WTM + i * 16 + (lane & 15)) * kBK;
+#pragma unroll
+  for (int i = 0; i < WTN; ++i) rowB[i] = (wn * 16 * WTN + i * 16 + (lane & 15)) * kBK;
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) sw[ks] = ((ks * 4 + (lane >> 4)) ^ (lane & 7)) << 3;
 
-  f32x4 acc[4][4];
+  f32x4 acc[WTM][WTN];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int i = 0; i < WTM; ++i)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < WTN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = p.K / kBK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int s = 0; s < nk; ++s) {
-    const int cur = s & 1;
-    if (s + 1 < nk) gload((s + 1) * kBK);
-    const uint16_t* as = sA[cur];
-    const uint16_t* bs = sB[cur];
+  auto multiply = [&](int buf) {
+    const uint16_t* as = sA + buf * BM * kBK;
+    const uint16_t* bs = sB + buf * BN * kBK;
+    // both k halves' fragments are read before the first MFMA, so the second half's reads are
+    // in flight while the first half's MFMAs issue
+    bf16x8 a[2][WTM], b[2][WTN];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 a[4], b[4];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        a[t] = *reinterpret_cast<const bf16x8*>(as + rowA[t] + sw[ks]);
-        b[t] = *reinterpret_cast<const bf16x8*>(bs + rowB[t] + sw[ks]);
-      }
+      for (int i = 0; i < WTM; ++i)
+        a[ks][i] = *reinterpret_cast<const bf16x8*>(as + rowA[i] + sw[ks]);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+      for (int j = 0; j < WTN; ++j)
+        b[ks][j] = *reinterpret_cast<const bf16x8*>(bs + rowB[j] + sw[ks]);
     }
-    if (s + 1 < nk) lstore(cur ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int i = 0; i < WTM; ++i)
+#pragma unroll
+        for (int j = 0; j < WTN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][j], acc[i][j], 0, 0, 0);
+  };
+  // Stage s sits in LDS buffer s % 2 and, until stored, in register set s % 2. The loads and
+  // stores are unconditional (the last two steps reload the final stage and store into the
+  // buffer nobody reads again): behind a branch, the compiler could no longer tell which loads
+  // are still in flight at the stores and would wait for all of them. The scheduling barriers
+  // keep the loads at the head of the step, ahead of the MFMAs (left alone, the scheduler sinks
+  // them below the MFMAs to save registers).
+  auto step = [&](auto& cur, auto& nxt, int s, int nk) {
+    gload(cur, (s + 2 < nk ? s + 2 : nk - 1) * kBK);
+    __builtin_amdgcn_sched_barrier(0);
+    multiply(s & 1);
+    __builtin_amdgcn_sched_barrier(0);
+    lstore(nxt, (s + 1) & 1);
     __syncthreads();
+  };
+  const int nk = p.K / kBK;  // even: K is a multiple of 128
+  if constexpr (WTM * WTN > 16) {
+    // large wave tiles: one register set, loaded one stage ahead (a stage's 2 * WTM * WTN MFMAs
+    // cover the load latency), which keeps the accumulators and fragments in registers
+    auto step1 = [&](int s) {
+      gload(g0, (s + 1 < nk ? s + 1 : nk - 1) * kBK);
+      __builtin_amdgcn_sched_barrier(0);
+      multiply(s & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      lstore(g0, (s + 1) & 1);
+      __syncthreads();
+    };
+    gload(g0, 0);
+    lstore(g0, 0);
+    __syncthreads();
+    for (int s = 0; s < nk; ++s) step1(s);
+  } else {
+    gload(g0, 0);
+    gload(g1, kBK);
+    lstore(g0, 0);
+    __syncthreads();
+    for (int s = 0; s < nk; s += 2) {
+      step(g0, g1, s, nk);
+      step(g1, g0, s + 1, nk);
+    }
   }
 
   // epilogue: lane holds rows 4 * (lane / 16) + j of each 16-row block, column lane % 16
-  const int64_t rbase = m0 + wm * 64 + 4 * (lane >> 4);
-  const int cbase = n0 + wn * 64 + (lane & 15);
+  const int64_t rbase = m0 + wm * 16 * WTM + 4 * (lane >> 4);
+  const int cbase = n0 + wn * 16 * WTN + (lane & 15);
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < WTM; ++mt)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int64_t row = rbase + mt * 16 + j;
       if (row >= p.M) continue;
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int col = cbase + nt * 16;
-        const float v = acc[mt][nt][j];
+      for (int nt2 = 0; nt2 < WTN; ++nt2) {
+        const int col = cbase + nt2 * 16;
+        const float v = acc[mt][nt2][j];
         if constexpr (MODE == kModeResid) {
           float* x = p.X + row * p.N + col;
           *x = *x + v;
@@ -230,6 +296,27 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_bf16_kernel(GemmArgs p) {
     }
 }
 
+template <int MODE, int WTM, int WTN>
+void launch_gemm_tile(const GemmArgs& a, hipStream_t stream) {
+  constexpr int BM = 32 * WTM, BN = 32 * WTN;
+  constexpr size_t lds = (size_t)2 * (BM + BN) * kBK * 2;
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(gemm_bf16_kernel<MODE, WTM, WTN>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  (void)attr;
+  const int64_t tiles = (a.M + BM - 1) / BM * (a.N / BN);
+  hipLaunchKernelGGL((gemm_bf16_kernel<MODE, WTM, WTN>), dim3((unsigned)tiles),
+                     dim3(kGemmThreads), lds, stream, a);
+}
+
+// 128 x 128 tiles (64 x 64 per wave): two workgroups per compute unit, so one's barrier waits
+// and epilogue overlap the other's MFMAs (256 x 256 tiles at one wave per SIMD measured 1.3-4.6x
+// slower)
+template <int MODE>
+void launch_gemm(const GemmArgs& a, hipStream_t stream) {
+  launch_gemm_tile<MODE, 4, 4>(a, stream);
+}
+
 // ---- lattice attention ----------------------------------------------------------------------
 struct AttnArgs {
   const uint16_t* qk;    // [N * L][2H]: Q at column h * 128, K at H + h * 128
@@ -240,11 +327,20 @@ struct AttnArgs {
   int S, K, L, Lv, Lp, H, heads;
 };
 
+// Lattices with S * Lp <= kBiasRows keep one row of additive logit bias per query slot in LDS
+// (slot-distance and same-slot terms in log2 units, -inf past the last key); larger ones look the
+// bias up per element.
+constexpr int kBiasRows = 4096;
+
+inline bool attn_bias_rows(int Lp, int S) { return (int64_t)S * Lp <= kBiasRows; }
+
 inline size_t attn_lds_bytes(int Lp, int S) {
   return (size_t)Lp * kHd * 2 + (size_t)kHd * (Lp + 4) * 2 + (size_t)((2 * S + 3) & ~3) * 4 +
-         (size_t)Lp * 4;
+         (size_t)Lp * 4 + (attn_bias_rows(Lp, S) ? (size_t)S * Lp * 4 : 0);
 }
 
+// NT = Lp / 16 key tiles (even, 2..16): the key loops are unrolled exactly.
+template <bool ROWS, int NT>
 __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int n = blockIdx.x / p.heads, h = blockIdx.x - n * p.heads;
@@ -254,44 +350,16 @@ __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArg
   uint16_t* sV = sK + Lp * kHd;                              // [128][Lp + 4]
   float* sBias = reinterpret_cast<float*>(sV + kHd * vstride);  // [2S - 1] dist, [2S - 1] same (log2 units)
   int* sSlot = reinterpret_cast<int*>(sBias + ((2 * p.S + 3) & ~3));  // [Lp] key slot, -1 past L
+  float* sRow = reinterpret_cast<float*>(sSlot + Lp);  // ROWS: [S][Lp] bias of query slot x key
   const int64_t tok0 = (int64_t)n * L;
   const int H2 = 2 * p.H;
 
-  for (int i = tid; i < Lp * 16; i += kAttnThreads) {
-    const int j = i >> 4, c = i & 15;
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (j < L)
-      v = *reinterpret_cast<const u32x4*>(p.qk + (tok0 + j) * H2 + p.H + h * kHd + c * 8);
-    *reinterpret_cast<u32x4*>(sK + j * kHd + ((c ^ (j & 7)) << 3)) = v;
-  }
-  const int cpr = Lp / 8;
-  for (int i = tid; i < kHd * cpr; i += kAttnThreads) {
-    const int c = i / cpr, pos = (i - c * cpr) * 8;
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (pos < p.Lv)
-      v = *reinterpret_cast<const u32x4*>(p.vt + ((int64_t)n * p.H + h * kHd + c) * p.Lv + pos);
-    if (pos + 8 > L) {  // keys past L must contribute exactly zero
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (pos + e >= L) v[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-    }
-    u32x2* dst = reinterpret_cast<u32x2*>(sV + c * vstride + pos);
-    dst[0] = u32x2{v.x, v.y};
-    dst[1] = u32x2{v.z, v.w};
-  }
-  const int nb = 2 * p.S - 1;
-  for (int i = tid; i < nb; i += kAttnThreads) sBias[i] = p.dist[(int64_t)h * nb + i] * kLog2e;
-  if (tid == 0) sBias[nb] = p.same[h] * kLog2e;
-  for (int i = tid; i < Lp; i += kAttnThreads) sSlot[i] = i < L ? i / p.K : -1;
-  __syncthreads();
-
-  const float zscale = kLog2e * 0.08838834764831845f;  // log2(e) / sqrt(128)
-  const float same_b = sBias[nb];
-  const int nq = (L + 15) / 16, ntile = Lp / 16;
   const int g = lane >> 4, c16 = lane & 15;
-  for (int qc = wave; qc < nq; qc += kAttnThreads / 64) {
+  const int nq = (L + 15) / 16;
+  // Q fragments of this wave's first query chunk, loaded while K and V^T are staged
+  bf16x8 qf[4];
+  auto load_q = [&](int qc) {
     const int q = qc * 16 + c16;
-    bf16x8 qf[4];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       u32x4 v = u32x4{0u, 0u, 0u, 0u};
@@ -299,35 +367,112 @@ __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArg
         v = *reinterpret_cast<const u32x4*>(p.qk + (tok0 + q) * H2 + h * kHd + ks * 32 + g * 8);
       qf[ks] = __builtin_bit_cast(bf16x8, v);
     }
-    // logits of query q (this lane's column) against keys 16t + 4g + i
-    f32x4 s[kMaxL / 16];
+  };
+  if (wave < nq) load_q(wave);
+
+  // K rows (16 chunks of 16 bytes each) and V^T rows (Lp / 8 chunks each), staged with
+  // kStage loads in flight per thread
+  constexpr int kStage = 8;
+  const int cpr = Lp / 8;
+  const int nK = Lp * 16, nKV = nK + kHd * cpr;
+  for (int base = tid; base < nKV; base += kStage * kAttnThreads) {
+    u32x4 v[kStage];
 #pragma unroll
-    for (int t = 0; t < kMaxL / 16; ++t) {
-      s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (t < ntile) {
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              sK + (t * 16 + c16) * kHd + (((ks * 4 + g) ^ (c16 & 7)) << 3));
-          s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ks], s[t], 0, 0, 0);
-        }
+    for (int b = 0; b < kStage; ++b) {
+      const int i = base + b * kAttnThreads;
+      v[b] = u32x4{0u, 0u, 0u, 0u};
+      if (i < nK) {
+        const int j = i >> 4, c = i & 15;
+        if (j < L)
+          v[b] = *reinterpret_cast<const u32x4*>(p.qk + (tok0 + j) * H2 + p.H + h * kHd + c * 8);
+      } else if (i < nKV) {
+        const int c = (i - nK) / cpr, pos = (i - nK - c * cpr) * 8;
+        if (pos < p.Lv)
+          v[b] = *reinterpret_cast<const u32x4*>(p.vt + ((int64_t)n * p.H + h * kHd + c) * p.Lv +
+                                                 pos);
       }
     }
+#pragma unroll
+    for (int b = 0; b < kStage; ++b) {
+      const int i = base + b * kAttnThreads;
+      if (i < nK) {
+        const int j = i >> 4, c = i & 15;
+        *reinterpret_cast<u32x4*>(sK + j * kHd + ((c ^ (j & 7)) << 3)) = v[b];
+      } else if (i < nKV) {
+        const int c = (i - nK) / cpr, pos = (i - nK - c * cpr) * 8;
+        u32x4 w = v[b];
+        if (pos + 8 > L) {  // keys past L must contribute exactly zero
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (pos + e >= L) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+        }
+        u32x2* dst = reinterpret_cast<u32x2*>(sV + c * vstride + pos);
+        dst[0] = u32x2{w.x, w.y};
+        dst[1] = u32x2{w.z, w.w};
+      }
+    }
+  }
+  const int nb = 2 * p.S - 1;
+  for (int i = tid; i < nb; i += kAttnThreads) sBias[i] = p.dist[(int64_t)h * nb + i] * kLog2e;
+  if (tid == 0) sBias[nb] = p.same[h] * kLog2e;
+  for (int i = tid; i < Lp; i += kAttnThreads) sSlot[i] = i < L ? i / p.K : -1;
+  if constexpr (ROWS) {
+    for (int i = tid; i < p.S * Lp; i += kAttnThreads) {
+      const int sq = i / Lp, key = i - sq * Lp;
+      float b = -__builtin_inff();
+      if (key < L) {
+        const int d = sq - key / p.K;
+        b = p.dist[(int64_t)h * nb + d + p.S - 1] * kLog2e + (d == 0 ? p.same[h] * kLog2e : 0.f);
+      }
+      sRow[i] = b;
+    }
+  }
+  __syncthreads();
+
+  const float zscale = kLog2e * 0.08838834764831845f;  // log2(e) / sqrt(128)
+  const float same_b = sBias[nb];
+  constexpr int kWaves = kAttnThreads / 64;
+  for (int qc = wave; qc < nq; qc += kWaves) {
+    const int q = qc * 16 + c16;
+    // logits of query q (this lane's column) against keys 16t + 4g + i
+    f32x4 s[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+            sK + (t * 16 + c16) * kHd + (((ks * 4 + g) ^ (c16 & 7)) << 3));
+        s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[ks], s[t], 0, 0, 0);
+      }
+      // one tile's fragments at a time (hoisting every tile's reads would take 4 NT registers)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (qc + kWaves < nq) load_q(qc + kWaves);  // the next chunk's fragments, in flight
     const int sq = q < L ? q / p.K : 0;
     float mx = -__builtin_inff();
 #pragma unroll
-    for (int t = 0; t < kMaxL / 16; ++t) {
-      if (t < ntile) {
-        const i32x4 sk = *reinterpret_cast<const i32x4*>(sSlot + t * 16 + 4 * g);
+    for (int t = 0; t < NT; ++t) {
+      {
+        if constexpr (ROWS) {
+          const f32x4 b = *reinterpret_cast<const f32x4*>(sRow + sq * Lp + t * 16 + 4 * g);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float z = -__builtin_inff();
-          if (sk[i] >= 0) {
-            const int d = sq - sk[i];
-            z = s[t][i] * zscale + sBias[d + p.S - 1] + (d == 0 ? same_b : 0.f);
+          for (int i = 0; i < 4; ++i) {
+            s[t][i] = fmaf(s[t][i], zscale, b[i]);
+            mx = fmaxf(mx, s[t][i]);
           }
-          s[t][i] = z;
-          mx = fmaxf(mx, z);
+        } else {
+          const i32x4 sk = *reinterpret_cast<const i32x4*>(sSlot + t * 16 + 4 * g);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float z = -__builtin_inff();
+            if (sk[i] >= 0) {
+              const int d = sq - sk[i];
+              z = s[t][i] * zscale + sBias[d + p.S - 1] + (d == 0 ? same_b : 0.f);
+            }
+            s[t][i] = z;
+            mx = fmaxf(mx, z);
+          }
         }
       }
     }
@@ -335,11 +480,11 @@ __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArg
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     float sum = 0.f;
 #pragma unroll
-    for (int t = 0; t < kMaxL / 16; ++t) {
-      if (t < ntile) {
+    for (int t = 0; t < NT; ++t) {
+      {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float e = exp2f(s[t][i] - mx);
+          const float e = __builtin_amdgcn_exp2f(s[t][i] - mx);
           s[t][i] = e;
           sum += e;
         }
@@ -349,37 +494,68 @@ __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArg
     sum += __shfl_xor(sum, 32, 64);
     const float rs = 1.0f / sum;
 
+    // O^T = V^T P^T: the V^T rows (head dimensions) are the MFMA rows and the probabilities of
+    // this lane's query the columns, so each lane ends with four consecutive dimensions of one
+    // query (one 8-byte store per 16-dimension tile)
     f32x4 o[kHd / 16];
 #pragma unroll
     for (int dt = 0; dt < kHd / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < kMaxL / 32; ++u) {
-      if (2 * u < ntile) {
-        const u32x4 pw = u32x4{pack_bf16x2(s[2 * u][0] * rs, s[2 * u][1] * rs),
-                               pack_bf16x2(s[2 * u][2] * rs, s[2 * u][3] * rs),
-                               pack_bf16x2(s[2 * u + 1][0] * rs, s[2 * u + 1][1] * rs),
-                               pack_bf16x2(s[2 * u + 1][2] * rs, s[2 * u + 1][3] * rs)};
-        const bf16x8 pa = __builtin_bit_cast(bf16x8, pw);
+    for (int u = 0; u < NT / 2; ++u) {
+      const u32x4 pw = u32x4{pack_bf16x2(s[2 * u][0] * rs, s[2 * u][1] * rs),
+                             pack_bf16x2(s[2 * u][2] * rs, s[2 * u][3] * rs),
+                             pack_bf16x2(s[2 * u + 1][0] * rs, s[2 * u + 1][1] * rs),
+                             pack_bf16x2(s[2 * u + 1][2] * rs, s[2 * u + 1][3] * rs)};
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
-        for (int dt = 0; dt < kHd / 16; ++dt) {
-          const uint16_t* vr = sV + (dt * 16 + c16) * vstride + u * 32 + 4 * g;
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vr + 16);
-          const bf16x8 vb = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
-          o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[dt], 0, 0, 0);
-        }
+      for (int dt = 0; dt < kHd / 16; ++dt) {
+        const uint16_t* vr = sV + (dt * 16 + c16) * vstride + u * 32 + 4 * g;
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
+        const u32x2 hi = *reinterpret_cast<const u32x2*>(vr + 16);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, o[dt], 0, 0, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // lane holds queries qc * 16 + 4g + i, head dimension dt * 16 + c16
+    // lane holds query qc * 16 + c16, head dimensions dt * 16 + 4g + i
+    if (q < L) {
+      u32x2* dst = reinterpret_cast<u32x2*>(p.out + (tok0 + q) * p.H + h * kHd + 4 * g);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int qq = qc * 16 + 4 * g + i;
-      if (qq >= L) continue;
-      uint16_t* dst = p.out + (tok0 + qq) * p.H + h * kHd + c16;
-#pragma unroll
-      for (int dt = 0; dt < kHd / 16; ++dt) dst[dt * 16] = (uint16_t)bf16_rne(o[dt][i]);
+      for (int dt = 0; dt < kHd / 16; ++dt)
+        dst[dt * 4] = u32x2{pack_bf16x2(o[dt][0], o[dt][1]), pack_bf16x2(o[dt][2], o[dt][3])};
     }
   }
+}
+
+template <bool ROWS, int NT>
+void launch_attention_nt(const AttnArgs& at, int64_t N, size_t lds, hipStream_t stream) {
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(lattice_attention_kernel<ROWS, NT>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  (void)attr;
+  hipLaunchKernelGGL((lattice_attention_kernel<ROWS, NT>), dim3((unsigned)(N * at.heads)),
+                     dim3(kAttnThreads), lds, stream, at);
+}
+
+template <bool ROWS>
+void launch_attention_rows(const AttnArgs& at, int64_t N, size_t lds, hipStream_t stream) {
+  switch (at.Lp / 16) {
+    case 2: launch_attention_nt<ROWS, 2>(at, N, lds, stream); break;
+    case 4: launch_attention_nt<ROWS, 4>(at, N, lds, stream); break;
+    case 6: launch_attention_nt<ROWS, 6>(at, N, lds, stream); break;
+    case 8: launch_attention_nt<ROWS, 8>(at, N, lds, stream); break;
+    case 10: launch_attention_nt<ROWS, 10>(at, N, lds, stream); break;
+    case 12: launch_attention_nt<ROWS, 12>(at, N, lds, stream); break;
+    case 14: launch_attention_nt<ROWS, 14>(at, N, lds, stream); break;
+    default: launch_attention_nt<ROWS, 16>(at, N, lds, stream); break;
+  }
+}
+
+void launch_attention(const AttnArgs& at, int64_t N, size_t lds, hipStream_t stream) {
+  if (attn_bias_rows(at.Lp, at.S))
+    launch_attention_rows<true>(at, N, lds, stream);
+  else
+    launch_attention_rows<false>(at, N, lds, stream);
 }
 
 // ---- packing ------------------------------------------------------------------------------------
@@ -446,12 +622,6 @@ inline bool forward_sizes_ok(int64_t N, int64_t S, int K, int H, int F) {
   return M * widest * 4 < ((int64_t)1 << 31);
 }
 
-template <int MODE>
-void launch_gemm(const GemmArgs& a, hipStream_t stream) {
-  const int64_t tiles = (a.M + kBM - 1) / kBM * (a.N / kBN);
-  hipLaunchKernelGGL(gemm_bf16_kernel<MODE>, dim3((unsigned)tiles), dim3(kGemmThreads), 0, stream,
-                     a);
-}
 
 void launch_rmsnorm(const float* X, const float* g, uint16_t* Y, int64_t M, int H,
                     hipStream_t stream) {
@@ -539,10 +709,7 @@ extern "C" lilicorr_status lilicorr_scorer_forward(float* X, int64_t N, int64_t 
   at.S = (int)S; at.K = K; at.L = L; at.Lv = w.Lv; at.Lp = (L + 31) / 32 * 32; at.H = H;
   at.heads = heads;
   const size_t attn_lds = attn_lds_bytes(at.Lp, at.S);
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(lattice_attention_kernel),
-      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-  (void)attr;
+
 
   for (int li = 0; li < layers; ++li) {
     const unsigned char* lp = static_cast<const unsigned char*>(packed) + (size_t)li * pl.total;
@@ -560,8 +727,7 @@ extern "C" lilicorr_status lilicorr_scorer_forward(float* X, int64_t N, int64_t 
     g.A = xn; g.Bt = wqkv; g.M = M; g.K = H; g.N = 3 * H; g.Y = qk; g.Vt = vt; g.H = H; g.L = L;
     g.Lv = w.Lv;
     launch_gemm<kModeQKV>(g, stream);
-    hipLaunchKernelGGL(lattice_attention_kernel, dim3((unsigned)(N * heads)), dim3(kAttnThreads),
-                       attn_lds, stream, at);
+    launch_attention(at, N, attn_lds, stream);
     GemmArgs r{};
     r.A = ao; r.Bt = wo; r.M = M; r.K = H; r.N = H; r.X = X;
     launch_gemm<kModeResid>(r, stream);
