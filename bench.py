@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--no-stress", action="store_true", help="skip the stress logits-pass line")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-scorer", action="store_true",
+                    help="skip the scoring-Transformer stand-in line")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-workload line (both metrics at every workload)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -214,6 +216,40 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
             "blocks_s": N / step, "step_us": step * 1e6,
             "logits_GB_s": nbytes / t_topk / 1e9, "logits_us": t_topk * 1e6,
             "logits_frac_of_8TBs": nbytes / t_topk / 1e9 / PEAK_HBM_GBS}
+
+
+PEAK_BF16_TFLOPS = 2500.0
+
+
+def scorer_rate(L, torch, workloads, iters=50, warmup=10):
+    """The scoring-Transformer stand-in at the headline lattice (64 requests x 15 slots x 16
+    candidates, width 1024, 8 heads, feed-forward 2048, two layers): mean forward time over
+    back-to-back calls between two HIP events, and its matrix-core rate (algorithmic FLOPs: the
+    four GEMMs and both attention products)."""
+    sc = workloads.SCORER_HEADLINE
+    inp = workloads.make_scorer_inputs(sc)
+    layers = [{k: v.cuda() for k, v in l.items()} for l in inp["layers"]]
+    packed = L.scorer_pack(layers, sc.S)
+    X = inp["X"].cuda()
+    ws = L.scorer_workspace(sc.N, sc.S, sc.K, sc.H, sc.F)
+    fwd = lambda: L.scorer_forward(X, packed, sc.S, sc.K, sc.heads, sc.F, sc.layers, workspace=ws)
+    for _ in range(warmup):
+        fwd()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(iters):
+        fwd()
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / iters
+    M = sc.N * sc.L
+    flops = sc.layers * (2 * M * (4 * sc.H * sc.H + 2 * sc.H * sc.F)
+                         + sc.N * (sc.H // 128) * 4 * sc.L * sc.L * 128)
+    return {"workload": f"N={sc.N} requests, S={sc.S} slots x K={sc.K} candidates, H={sc.H}, "
+                        f"{sc.heads} heads, F={sc.F}, {sc.layers} layers, bf16 matrix cores",
+            "us_per_forward": us, "TFLOP_s": flops / us / 1e6, "GFLOP": flops / 1e9,
+            "frac_of_bf16_peak": flops / us / 1e6 / PEAK_BF16_TFLOPS}
 
 
 def cpu_baseline(cfg, inp, seconds):
@@ -442,6 +478,9 @@ def main():
             torch.cuda.empty_cache()
             print(f"[bench] workload {c.name} done", file=sys.stderr, flush=True)
         out["per_workload"] = per
+
+    if not args.no_scorer:
+        out["scorer"] = scorer_rate(L, torch, workloads)
 
     if args.calibrate_copy:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)

@@ -345,7 +345,8 @@ __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArg
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int n = blockIdx.x / p.heads, h = blockIdx.x - n * p.heads;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Lp = p.Lp, L = p.L, vstride = Lp + 4;
+  constexpr int Lp = 16 * NT, vstride = Lp + 4;
+  const int L = p.L;
   uint16_t* sK = reinterpret_cast<uint16_t*>(smem);        // [Lp][128], chunk c of key j at c ^ (j % 8)
   uint16_t* sV = sK + Lp * kHd;                              // [128][Lp + 4]
   float* sBias = reinterpret_cast<float*>(sV + kHd * vstride);  // [2S - 1] dist, [2S - 1] same (log2 units)
@@ -370,59 +371,64 @@ __global__ __launch_bounds__(kAttnThreads) void lattice_attention_kernel(AttnArg
   };
   if (wave < nq) load_q(wave);
 
-  // K rows (16 chunks of 16 bytes each) and V^T rows (Lp / 8 chunks each), staged with
-  // kStage loads in flight per thread
-  constexpr int kStage = 8;
-  const int cpr = Lp / 8;
-  const int nK = Lp * 16, nKV = nK + kHd * cpr;
-  for (int base = tid; base < nKV; base += kStage * kAttnThreads) {
-    u32x4 v[kStage];
+  // K rows (16 chunks of 16 bytes each) and V^T rows (Lp / 8 = 2 NT chunks each): NT / 2 chunks
+  // of each per thread, every load issued before the first LDS store
+  constexpr int kPer = NT / 2;  // (Lp * 16) / 512 == (128 * Lp / 8) / 512
+  constexpr int cpr = 2 * NT;
+  u32x4 kv[2 * kPer];
 #pragma unroll
-    for (int b = 0; b < kStage; ++b) {
-      const int i = base + b * kAttnThreads;
-      v[b] = u32x4{0u, 0u, 0u, 0u};
-      if (i < nK) {
-        const int j = i >> 4, c = i & 15;
-        if (j < L)
-          v[b] = *reinterpret_cast<const u32x4*>(p.qk + (tok0 + j) * H2 + p.H + h * kHd + c * 8);
-      } else if (i < nKV) {
-        const int c = (i - nK) / cpr, pos = (i - nK - c * cpr) * 8;
-        if (pos < p.Lv)
-          v[b] = *reinterpret_cast<const u32x4*>(p.vt + ((int64_t)n * p.H + h * kHd + c) * p.Lv +
-                                                 pos);
+  for (int b = 0; b < kPer; ++b) {
+    const int i = tid + b * kAttnThreads;
+    const int j = i >> 4, c = i & 15;
+    kv[b] = u32x4{0u, 0u, 0u, 0u};
+    if (j < L)
+      kv[b] = *reinterpret_cast<const u32x4*>(p.qk + (tok0 + j) * H2 + p.H + h * kHd + c * 8);
+  }
+#pragma unroll
+  for (int b = 0; b < kPer; ++b) {
+    const int i = tid + b * kAttnThreads;
+    const int c = i / cpr, pos = (i - c * cpr) * 8;
+    kv[kPer + b] = u32x4{0u, 0u, 0u, 0u};
+    if (pos < p.Lv)
+      kv[kPer + b] = *reinterpret_cast<const u32x4*>(
+          p.vt + ((int64_t)n * p.H + h * kHd + c) * p.Lv + pos);
+  }
+#pragma unroll
+  for (int b = 0; b < kPer; ++b) {
+    const int i = tid + b * kAttnThreads;
+    const int j = i >> 4, c = i & 15;
+    *reinterpret_cast<u32x4*>(sK + j * kHd + ((c ^ (j & 7)) << 3)) = kv[b];
+  }
+#pragma unroll
+  for (int b = 0; b < kPer; ++b) {
+    const int i = tid + b * kAttnThreads;
+    const int c = i / cpr, pos = (i - c * cpr) * 8;
+    u32x4 w = kv[kPer + b];
+    const int nv = L - pos;  // keys of this chunk inside the lattice; the rest must be zero
+    if (nv < 8) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t keep = (2 * e + 1 < nv) ? 0xffffffffu : (2 * e < nv ? 0x0000ffffu : 0u);
+        w[e] &= keep;
       }
     }
-#pragma unroll
-    for (int b = 0; b < kStage; ++b) {
-      const int i = base + b * kAttnThreads;
-      if (i < nK) {
-        const int j = i >> 4, c = i & 15;
-        *reinterpret_cast<u32x4*>(sK + j * kHd + ((c ^ (j & 7)) << 3)) = v[b];
-      } else if (i < nKV) {
-        const int c = (i - nK) / cpr, pos = (i - nK - c * cpr) * 8;
-        u32x4 w = v[b];
-        if (pos + 8 > L) {  // keys past L must contribute exactly zero
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (pos + e >= L) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-        }
-        u32x2* dst = reinterpret_cast<u32x2*>(sV + c * vstride + pos);
-        dst[0] = u32x2{w.x, w.y};
-        dst[1] = u32x2{w.z, w.w};
-      }
-    }
+    u32x2* dst = reinterpret_cast<u32x2*>(sV + c * vstride + pos);
+    dst[0] = u32x2{w.x, w.y};
+    dst[1] = u32x2{w.z, w.w};
   }
   const int nb = 2 * p.S - 1;
   for (int i = tid; i < nb; i += kAttnThreads) sBias[i] = p.dist[(int64_t)h * nb + i] * kLog2e;
   if (tid == 0) sBias[nb] = p.same[h] * kLog2e;
   for (int i = tid; i < Lp; i += kAttnThreads) sSlot[i] = i < L ? i / p.K : -1;
   if constexpr (ROWS) {
+    __syncthreads();  // the rows read the slot and bias tables
     for (int i = tid; i < p.S * Lp; i += kAttnThreads) {
       const int sq = i / Lp, key = i - sq * Lp;
+      const int sk = sSlot[key];
       float b = -__builtin_inff();
-      if (key < L) {
-        const int d = sq - key / p.K;
-        b = p.dist[(int64_t)h * nb + d + p.S - 1] * kLog2e + (d == 0 ? p.same[h] * kLog2e : 0.f);
+      if (sk >= 0) {
+        const int d = sq - sk;
+        b = sBias[d + p.S - 1] + (d == 0 ? sBias[nb] : 0.f);
       }
       sRow[i] = b;
     }
