@@ -268,32 +268,46 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_bf16_kernel(GemmArgs p) {
   // epilogue: lane holds rows 4 * (lane / 16) + j of each 16-row block, column lane % 16
   const int64_t rbase = m0 + wm * 16 * WTM + 4 * (lane >> 4);
   const int cbase = n0 + wn * 16 * WTN + (lane & 15);
+  const bool vpart = MODE == kModeQKV && n0 >= 2 * p.H;  // uniform: a tile is all Q/K or all V
 #pragma unroll
-  for (int mt = 0; mt < WTM; ++mt)
+  for (int mt = 0; mt < WTM; ++mt) {
+    // request and lattice position of the block's first row (rows < 2^31), then stepped
+    const int64_t row0 = rbase + mt * 16;
+    int rq = 0, l = 0;
+    if (vpart) {
+      rq = (int)row0 / p.L;
+      l = (int)row0 - rq * p.L;
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int64_t row = rbase + mt * 16 + j;
-      if (row >= p.M) continue;
+      const int64_t row = row0 + j;
+      if (row < p.M) {
 #pragma unroll
-      for (int nt2 = 0; nt2 < WTN; ++nt2) {
-        const int col = cbase + nt2 * 16;
-        const float v = acc[mt][nt2][j];
-        if constexpr (MODE == kModeResid) {
-          float* x = p.X + row * p.N + col;
-          *x = *x + v;
-        } else if constexpr (MODE == kModeSilu) {
-          p.Y[row * p.N + col] = (uint16_t)bf16_rne(v / (1.0f + __expf(-v)));
-        } else {
-          if (n0 < 2 * p.H) {
-            p.Y[row * (2 * p.H) + col] = (uint16_t)bf16_rne(v);
+        for (int nt2 = 0; nt2 < WTN; ++nt2) {
+          const int col = cbase + nt2 * 16;
+          const float v = acc[mt][nt2][j];
+          if constexpr (MODE == kModeResid) {
+            float* x = p.X + row * p.N + col;
+            *x = *x + v;
+          } else if constexpr (MODE == kModeSilu) {
+            // silu(v) = v / (1 + e^-v), the reciprocal on the hardware unit (the result is
+            // rounded to bf16 next)
+            p.Y[row * p.N + col] =
+                (uint16_t)bf16_rne(v * __builtin_amdgcn_rcpf(1.0f + __expf(-v)));
           } else {
-            const int64_t rq = row / p.L;
-            const int64_t l = row - rq * p.L;
-            p.Vt[(rq * p.H + (col - 2 * p.H)) * p.Lv + l] = (uint16_t)bf16_rne(v);
+            if (!vpart)
+              p.Y[row * (2 * p.H) + col] = (uint16_t)bf16_rne(v);
+            else
+              p.Vt[((int64_t)rq * p.H + (col - 2 * p.H)) * p.Lv + l] = (uint16_t)bf16_rne(v);
           }
         }
       }
+      if (vpart && ++l == p.L) {
+        l = 0;
+        ++rq;
+      }
     }
+  }
 }
 
 template <int MODE, int WTM, int WTN>
