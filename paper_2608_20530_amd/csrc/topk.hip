@@ -30,6 +30,7 @@
 //  * Rows split over several workgroups (small N*B) write partial results to the workspace and a
 //    second kernel merges them.
 #include <hip/hip_runtime.h>
+#include <climits>
 #include <math.h>
 #include <stdint.h>
 
@@ -693,33 +694,80 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
   }
 }
 
-// One wave per row: merge the `split` partial results of the row.
-__global__ __launch_bounds__(kWave) void topk_merge_kernel(const unsigned char* __restrict__ partials,
-                                                         int K, int split, int32_t* __restrict__ ids,
-                                                         float* __restrict__ logp,
-                                                         float* __restrict__ feat) {
-  const int lane = lane_id();
+// One workgroup of four waves per row merges the row's `split` (<= 256) partial results: thread
+// p reads partial p's (reference, exp sum) header and the workgroup reduces them; wave w merges
+// the key lists of partials w, w + 4, ..., with eight lists' loads in flight at a time, and wave
+// 0 merges the four results through LDS.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeBatch = 8;
+
+__global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
+    const unsigned char* __restrict__ partials, int K, int split, int32_t* __restrict__ ids,
+    float* __restrict__ logp, float* __restrict__ feat) {
+  __shared__ int sC[kMergeThreads / kWave];
+  __shared__ float sS[kMergeThreads / kWave];
+  __shared__ uint64_t sL[kMergeThreads / kWave][kWave];
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int64_t row = blockIdx.x;
+  const size_t stride = partial_stride(K);
+  const unsigned char* base = partials + (size_t)row * split * stride;
+
+  // reference: the largest valid one (no valid partial: reference 0, sum 0)
+  int cref = 0, valid = 0;
+  float s = 0.f;
+  if (tid < split) {
+    const Partial* hdr = reinterpret_cast<const Partial*>(base + (size_t)tid * stride);
+    valid = hdr->cvalid;
+    cref = hdr->cref;
+    s = hdr->s;
+  }
+  int c = valid ? cref : INT_MIN;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const int o = __shfl_xor(c, m, kWave);
+    c = o > c ? o : c;
+  }
+  if (lane == 0) sC[wave] = c;
+  __syncthreads();
+  int C = sC[0];
+#pragma unroll
+  for (int w = 1; w < kMergeThreads / kWave; ++w) C = sC[w] > C ? sC[w] : C;
+  if (C == INT_MIN) C = 0;
+  float part = valid ? ldexpf(s, cref - C) : 0.f;
+  part = wave_sum(part);
+  if (lane == 0) sS[wave] = part;
+
   uint64_t merged = 0;
-  int C = 0, any = 0;
-  for (int p = 0; p < split; ++p) {
-    const unsigned char* q = partials + ((size_t)row * split + p) * partial_stride(K);
-    const Partial* hdr = reinterpret_cast<const Partial*>(q);
-    if (hdr->cvalid) {
-      C = any ? (hdr->cref > C ? hdr->cref : C) : hdr->cref;
-      any = 1;
+  bool first = true;
+  for (int p0 = wave; p0 < split; p0 += kMergeBatch * (kMergeThreads / kWave)) {
+    uint64_t k[kMergeBatch];
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; ++b) {
+      const int p = p0 + b * (kMergeThreads / kWave);
+      k[b] = 0ull;
+      if (p < split && lane < K)
+        k[b] = reinterpret_cast<const uint64_t*>(base + (size_t)p * stride + sizeof(Partial))[lane];
+    }
+#pragma unroll
+    for (int b = 0; b < kMergeBatch; ++b) {
+      const int p = p0 + b * (kMergeThreads / kWave);
+      if (p < split) {
+        merged = first ? k[b] : merge_desc64(merged, k[b]);
+        first = false;
+      }
     }
   }
-  float S = 0.f;
-  for (int p = 0; p < split; ++p) {
-    const unsigned char* q = partials + ((size_t)row * split + p) * partial_stride(K);
-    const Partial* hdr = reinterpret_cast<const Partial*>(q);
-    const uint64_t* keys = reinterpret_cast<const uint64_t*>(q + sizeof(Partial));
-    if (hdr->cvalid) S += ldexpf(hdr->s, hdr->cref - C);
-    uint64_t k = lane < K ? keys[lane] : 0ull;
-    merged = p == 0 ? k : merge_desc64(merged, k);
+  sL[wave][lane] = merged;  // an empty list (all zero keys) when the wave had no partial
+  __syncthreads();
+  if (wave == 0) {
+    float S = sS[0];
+#pragma unroll
+    for (int w = 1; w < kMergeThreads / kWave; ++w) {
+      S += sS[w];
+      merged = merge_desc64(merged, sL[w][lane]);
+    }
+    write_row(merged, (log2((double)S) + (double)C) / (double)kLog2eF, row, K, ids, logp, feat);
   }
-  write_row(merged, (log2((double)S) + (double)C) / (double)kLog2eF, row, K, ids, logp, feat);
 }
 
 // Number of workgroups per row: enough workgroups to fill the chip (about four per CU), but
@@ -783,7 +831,7 @@ static lilicorr_status topk_launch(const void* logits, lilicorr_dtype dtype, int
                        logp, feat, ws);
   if (launch_status() != LILICORR_OK) return LILICORR_ERR_HIP;
   if (split > 1) {
-    hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)rows), dim3(kWave), 0, stream, ws, K, split,
+    hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)rows), dim3(kMergeThreads), 0, stream, ws, K, split,
                        ids, logp, feat);
     if (launch_status() != LILICORR_OK) return LILICORR_ERR_HIP;
   }
