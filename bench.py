@@ -279,6 +279,51 @@ def cpu_baseline(cfg, inp, seconds):
                       f"request, fp64, single thread), {dt:.1f} s"}
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline_threads(cfg, inp, seconds):
+    """The same oracle chain on every request of the workload, one request per task on a pool of
+    threads (the oracle's C routines release the interpreter lock), so it runs on the host's
+    cores; stops taking new requests after `seconds`."""
+    import concurrent.futures
+
+    import numpy as np
+
+    import oracle
+
+    lg = inp["logits"].view(__import__("torch").int16).numpy().view(np.uint16)
+    E = inp["E"].view(__import__("torch").int16).numpy().view(np.uint16)
+    W_in, W_out = inp["W_in"].numpy(), inp["W_out"].numpy()
+    oracle.topk(lg[:1, :1, :64], 4)
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    t0 = time.perf_counter()
+
+    def one(n):
+        if time.perf_counter() - t0 >= seconds:
+            return 0
+        ids, logp = oracle.topk(lg[n:n + 1], cfg.K)
+        iv, ov = oracle.candidate_vectors(ids, E, W_in, W_out)
+        S, S0 = oracle.pair_scores(iv, ov, None, 8.0)
+        oracle.greedy_walk(S, S0, logp, ids)
+        return 1
+
+    with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+        done = sum(ex.map(one, range(cfg.N)))
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "blocks/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {cfg.N} requests of the headline workload (whole chain per "
+                      f"request, fp64), one request per task on {threads} threads, {dt:.1f} s",
+            "cpu_model": cpu_model(), "nproc": os.cpu_count()}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -491,6 +536,8 @@ def main():
 
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, inp, args.cpu_seconds)
+        out["cpu_baseline"]["cpu_model"] = cpu_model()
+        out["cpu_baseline_all_cores"] = cpu_baseline_threads(cfg, inp, args.cpu_seconds)
 
     print(json.dumps(out), flush=True)
 
