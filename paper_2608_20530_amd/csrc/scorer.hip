@@ -326,9 +326,195 @@ void launch_gemm_tile(const GemmArgs& a, hipStream_t stream) {
 // 128 x 128 tiles (64 x 64 per wave): two workgroups per compute unit, so one's barrier waits
 // and epilogue overlap the other's MFMAs (256 x 256 tiles at one wave per SIMD measured 1.3-4.6x
 // slower)
+// ---- 128 x 256 tiles, operands by DMA ---------------------------------------------------------
+// Four waves (2 x 2), each a 64 x 128 block (32 accumulator tiles): a fragment read feeds 4 or 8
+// MFMAs, 12 KB of LDS reads per 32 MFMAs instead of 8 KB per 16. The operands reach LDS by DMA
+// (buffer loads with an LDS destination, lane i of a load writing 16 bytes at 16 i past the
+// wave's base), in a ring of three 32-deep stages (72 KB, two workgroups per compute unit); a
+// stage row is 64 bytes and chunk c of row r sits at position c ^ ((r / 2) % 4).
+constexpr int kDBK = 32;
+constexpr int kDA = 128 * kDBK, kDB = 256 * kDBK;  // elements of one stage of A, of B
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <int MODE>
+__global__ __launch_bounds__(kGemmThreads, 2) void gemm_dma_kernel(GemmArgs p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char dma_smem[];
+  uint16_t* ring = reinterpret_cast<uint16_t*>(dma_smem);  // [3][A stage, B stage]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int ntn = p.N / 256;
+  const uint32_t nt = gridDim.x;
+  const uint32_t t = (nt % 8u == 0u) ? (blockIdx.x % 8u) * (nt / 8u) + blockIdx.x / 8u
+                                     : blockIdx.x;
+  const int64_t ntm = (p.M + 127) / 128;
+  const int64_t per_group = (int64_t)kGroup * ntn;
+  const int64_t grp = t / per_group;
+  const int64_t rows_in = (ntm - grp * kGroup) < kGroup ? (ntm - grp * kGroup) : kGroup;
+  const int64_t r = t - grp * per_group;
+  const int64_t m0 = (grp * kGroup + r % rows_in) * 128;
+  const int n0 = (int)(r / rows_in) * 256;
+  const uint32_t K2 = (uint32_t)p.K * 2u;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.A, (uint32_t)p.M * K2);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(p.Bt, (uint32_t)p.N * K2);
+  // DMA slots: A has 512 (wave w: 128 w .. 128 w + 127, two loads), B 1024 (four loads)
+  uint32_t offA[2], offB[4];
+#pragma unroll
+  for (int d = 0; d < 2; ++d) {
+    const int q = wave * 128 + d * 64 + lane;
+    const int row = q >> 2, kc = (q & 3) ^ ((row >> 1) & 3);
+    offA[d] = (uint32_t)(m0 + row) * K2 + (uint32_t)kc * 16u;
+  }
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const int q = wave * 256 + d * 64 + lane;
+    const int row = q >> 2, kc = (q & 3) ^ ((row >> 1) & 3);
+    offB[d] = (uint32_t)(n0 + row) * K2 + (uint32_t)kc * 16u;
+  }
+  auto dma = [&](int buf, int stage) {
+    uint16_t* da = ring + buf * (kDA + kDB);
+    uint16_t* db = da + kDA;
+    const int soff = stage * kDBK * 2;
+#pragma unroll
+    for (int d = 0; d < 2; ++d)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ra, (lds_ptr_t)(da + (wave * 128 + d * 64) * 8), 16, offA[d], soff, 0, 0);
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rb, (lds_ptr_t)(db + (wave * 256 + d * 64) * 8), 16, offB[d], soff, 0, 0);
+  };
+  int rowA[4], rowB[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int x = wm * 64 + i * 16 + (lane & 15);
+    rowA[i] = x * kDBK + (((lane >> 4) ^ ((x >> 1) & 3)) << 3);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int x = wn * 128 + i * 16 + (lane & 15);
+    rowB[i] = x * kDBK + (((lane >> 4) ^ ((x >> 1) & 3)) << 3);
+  }
+  f32x4 acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto multiply = [&](int buf) {
+    const uint16_t* as = ring + buf * (kDA + kDB);
+    const uint16_t* bs = as + kDA;
+    bf16x8 a[4], b[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8*>(as + rowA[i]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b[j] = *reinterpret_cast<const bf16x8*>(bs + rowB[j]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  };
+  // the bare s_barrier after the wave's own DMA wait (six loads per stage per wave: stage s + 1
+  // has landed when only stage s + 2's six are in flight); __syncthreads() would add a release
+  // fence waiting for every DMA
+  const int nk = p.K / kDBK;  // a multiple of 4
+  dma(0, 0);
+  dma(1, 1);
+  __asm__ volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+  int s = 0;
+  for (; s + 3 <= nk; s += 3) {
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+      dma((u + 2) % 3, s + u + 2 < nk ? s + u + 2 : nk - 1);
+      multiply(u);
+      __asm__ volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+    }
+  }
+  for (int u = 0; s < nk; ++s, ++u) {
+    dma((u + 2) % 3, s + 2 < nk ? s + 2 : nk - 1);
+    multiply(u);
+    __asm__ volatile("s_waitcnt vmcnt(6)\n\ts_barrier" ::: "memory");
+  }
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // epilogue: lane holds rows 4 * (lane / 16) + j of each 16-row block, column lane % 16
+  const int64_t rbase = m0 + wm * 64 + 4 * (lane >> 4);
+  const int cbase = n0 + wn * 128 + (lane & 15);
+  const bool vpart = MODE == kModeQKV && n0 >= 2 * p.H;
+  // four consecutive rows of one request when L % 4 == 0 (a block's rows start at a multiple of
+  // 4): one 8-byte store per column into V^T
+  const bool vfast = vpart && (p.L % 4 == 0);
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt) {
+    const int64_t row0 = rbase + mt * 16;
+    if (vfast) {
+      if (row0 < p.M) {
+        const int rq4 = (int)row0 / p.L, l4 = (int)row0 - rq4 * p.L;
+#pragma unroll
+        for (int nt2 = 0; nt2 < 8; ++nt2) {
+          const int col = cbase + nt2 * 16;
+          *reinterpret_cast<u32x2*>(p.Vt + ((int64_t)rq4 * p.H + (col - 2 * p.H)) * p.Lv + l4) =
+              u32x2{pack_bf16x2(acc[mt][nt2][0], acc[mt][nt2][1]),
+                    pack_bf16x2(acc[mt][nt2][2], acc[mt][nt2][3])};
+        }
+      }
+      continue;
+    }
+    int rq = 0, l = 0;
+    if (vpart) {
+      rq = (int)row0 / p.L;
+      l = (int)row0 - rq * p.L;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t row = row0 + j;
+      if (row < p.M) {
+#pragma unroll
+        for (int nt2 = 0; nt2 < 8; ++nt2) {
+          const int col = cbase + nt2 * 16;
+          const float v = acc[mt][nt2][j];
+          if constexpr (MODE == kModeResid) {
+            float* x = p.X + row * p.N + col;
+            *x = *x + v;
+          } else if constexpr (MODE == kModeSilu) {
+            p.Y[row * p.N + col] =
+                (uint16_t)bf16_rne(v * __builtin_amdgcn_rcpf(1.0f + __expf(-v)));
+          } else {
+            if (!vpart)
+              p.Y[row * (2 * p.H) + col] = (uint16_t)bf16_rne(v);
+            else
+              p.Vt[((int64_t)rq * p.H + (col - 2 * p.H)) * p.Lv + l] = (uint16_t)bf16_rne(v);
+          }
+        }
+      }
+      if (vpart && ++l == p.L) {
+        l = 0;
+        ++rq;
+      }
+    }
+  }
+}
+
+template <int MODE>
+void launch_gemm_dma(const GemmArgs& a, hipStream_t stream) {
+  constexpr size_t lds = (size_t)3 * (kDA + kDB) * 2;
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(gemm_dma_kernel<MODE>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  (void)attr;
+  const int64_t tiles = (a.M + 127) / 128 * (a.N / 256);
+  hipLaunchKernelGGL(gemm_dma_kernel<MODE>, dim3((unsigned)tiles), dim3(kGemmThreads), lds,
+                     stream, a);
+}
+
+// 128 x 256 DMA-fed tiles when the output width allows, else 128 x 128
 template <int MODE>
 void launch_gemm(const GemmArgs& a, hipStream_t stream) {
-  launch_gemm_tile<MODE, 4, 4>(a, stream);
+  if (a.N % 256 == 0)
+    launch_gemm_dma<MODE>(a, stream);
+  else
+    launch_gemm_tile<MODE, 4, 4>(a, stream);
 }
 
 // ---- lattice attention ----------------------------------------------------------------------
