@@ -26,6 +26,7 @@
 // of another candidate and records the contenders; in step 6 the last workgroup decides each
 // flagged row it meets on the path again in double precision (certify.hpp).
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <math.h>
 #include <stdint.h>
 
@@ -38,8 +39,9 @@
 namespace lilicorr {
 namespace {
 
-constexpr int kSideRows = 64;                // candidate rows per side per workgroup
-constexpr int kSideRm = kSideRows / 16;      // 16-row blocks per side
+// Candidate rows per side per workgroup (SR): 64, or 32 / 16 when a batch is too small to give
+// every compute unit a workgroup at 64 (a workgroup then holds fewer slot pairs, P = SR / K).
+constexpr int kFillWorkgroups = 256;
 constexpr int kFusedMaxD = 256;              // the fp32 projections of both sides fit in LDS
 constexpr int64_t kMaxTableRows = 16384;     // a request's table is staged in LDS at the end
 constexpr int64_t kMaxExactSlots = 8192;     // exact decode: B bytes of path in LDS
@@ -48,6 +50,7 @@ constexpr size_t kExactStageBytes = 64 * 1024;    // exact decode: S[n] staged w
 constexpr size_t kCounterBytes = 256;        // counters are padded to this alignment
 
 struct FusedPlan {
+  int sr;            // candidate rows per side per workgroup (64, 32 or 16; K <= sr)
   int P;             // slot pairs per workgroup
   int groups;        // pair groups per request
   int wg;            // workgroups per request (pair groups + the anchor's)
@@ -62,19 +65,20 @@ struct FusedPlan {
   size_t lds_bytes;  // total dynamic LDS
 };
 
-inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = false) {
+inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = false, int sr = 64) {
   FusedPlan p;
+  p.sr = sr;
   p.cert_off = 0;
   const VecGeom g = vec_geom(d);
-  p.P = kSideRows / K;
+  p.P = sr / K;
   const int64_t pairs = B - 1;
   p.groups = pairs > 0 ? (int)((pairs + p.P - 1) / p.P) : 1;
   p.wg = p.groups;  // the anchor workgroup is added by the caller when present
   p.ws = g.waves;
   p.astride = g.dkp * 32 + 8;
   p.vstride = d + 4;
-  const size_t a_bytes = (size_t)2 * kSideRows * p.astride * 2;
-  const size_t v_bytes = (size_t)2 * kSideRows * p.vstride * 4;
+  const size_t a_bytes = (size_t)2 * sr * p.astride * 2;
+  const size_t v_bytes = (size_t)2 * sr * p.vstride * 4;
   size_t t_bytes;
   if (exact) {
     p.rows = (B - 1) * K * K + K;
@@ -95,9 +99,9 @@ inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = fal
   p.x_bytes = a_bytes > v_bytes ? a_bytes : v_bytes;
   if (t_bytes > p.x_bytes) p.x_bytes = t_bytes;
   p.x_bytes = (p.x_bytes + 15) / 16 * 16;
-  p.lds_bytes = p.x_bytes + (size_t)2 * p.ws * kSideRows * 4  // per-wave partial norms
-                + (size_t)2 * kSideRows * 4                   // row squared norms
-                + (size_t)2 * kSideRows * 4                   // row token ids
+  p.lds_bytes = p.x_bytes + (size_t)2 * p.ws * sr * 4  // per-wave partial norms
+                + (size_t)2 * sr * 4                   // row squared norms
+                + (size_t)2 * sr * 4                   // row token ids
                 + (size_t)p.P * K * K * 4                     // this workgroup's scores
                 + 16;                                         // ticket flag
   return p;
@@ -122,7 +126,7 @@ __device__ __forceinline__ void exchange_store(T* p, T v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int G, bool EXACT, bool CERT>
+template <int G, bool EXACT, bool CERT, int SR>
 __global__ __launch_bounds__(512) void score_walk_kernel(
     const int32_t* __restrict__ ids, const float* __restrict__ logp,
     const uint16_t* __restrict__ E, int64_t V, int d, const unsigned char* __restrict__ frags,
@@ -132,8 +136,9 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
     float* __restrict__ score, uint32_t* __restrict__ counters, void* __restrict__ exchange,
     float margin, const float* __restrict__ w32, uint64_t* __restrict__ cmask,
     int32_t* __restrict__ rescored) {
+  constexpr int kSideRows = SR, kSideRm = SR / 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [128][astride] gathered rows
+  uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [2 SR][astride] gathered rows
   float* Vf = reinterpret_cast<float*>(smem);       // [128][vstride] projections (after A)
   uint64_t* tbl = reinterpret_cast<uint64_t*>(smem);  // [rows] the request's table (last wg)
   uint64_t* table = static_cast<uint64_t*>(exchange);   // greedy: [N][rows] table entries
@@ -457,14 +462,24 @@ void launch_fused(const FusedPlan& plan, int64_t N, hipStream_t stream, const in
                   int K, float sigma, float lambda, float* S, float* S0, int32_t* draft,
                   int32_t* choice, float* logq, float* score, uint32_t* counters,
                   void* exchange, const CertArgs& ca) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(score_walk_kernel<G, EXACT, CERT>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-  (void)attr;
-  hipLaunchKernelGGL((score_walk_kernel<G, EXACT, CERT>), dim3((unsigned)(N * plan.wg)),
-                     dim3(2 * plan.ws * kWave), plan.lds_bytes, stream, ids, logp, E, V, d, frags,
-                     nbp, dkp, anchor_out, B, K, sigma, lambda, plan, S, S0, draft, choice, logq,
-                     score, counters, exchange, ca.margin, ca.w32, ca.cmask, ca.rescored);
+  auto go = [&](auto sr_const) {
+    constexpr int SR = decltype(sr_const)::value;
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(score_walk_kernel<G, EXACT, CERT, SR>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)attr;
+    hipLaunchKernelGGL((score_walk_kernel<G, EXACT, CERT, SR>), dim3((unsigned)(N * plan.wg)),
+                       dim3(2 * plan.ws * kWave), plan.lds_bytes, stream, ids, logp, E, V, d,
+                       frags, nbp, dkp, anchor_out, B, K, sigma, lambda, plan, S, S0, draft,
+                       choice, logq, score, counters, exchange, ca.margin, ca.w32, ca.cmask,
+                       ca.rescored);
+  };
+  // K <= G <= SR: the instances with SR below G are never launched
+  if constexpr (G <= 16)
+    if (plan.sr == 16) return go(std::integral_constant<int, 16>{});
+  if constexpr (G <= 32)
+    if (plan.sr == 32) return go(std::integral_constant<int, 32>{});
+  go(std::integral_constant<int, 64>{});
 }
 
 inline bool fused_shape_ok(int64_t N, int64_t B, int K, bool exact) {
@@ -496,7 +511,13 @@ lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const vo
       (rescored && !aligned16(rescored)))
     return LILICORR_ERR_ALIGNMENT;
   if (workspace_bytes < fused_workspace_bytes(N, B, K, EXACT, CERT)) return LILICORR_ERR_WORKSPACE;
-  FusedPlan plan = fused_plan(B, K, d, EXACT, CERT);
+  // the largest rows-per-side that still gives the chip kFillWorkgroups workgroups (or 16 rows,
+  // the smallest block, when even that does not); never below K
+  int sr = 64;
+  while (sr > 16 && sr / 2 >= K &&
+         N * (fused_plan(B, K, d, EXACT, CERT, sr).wg + (anchor_out ? 1 : 0)) < kFillWorkgroups)
+    sr /= 2;
+  FusedPlan plan = fused_plan(B, K, d, EXACT, CERT, sr);
   if (anchor_out) plan.wg += 1;
   if (N > 0x7fffffffll / plan.wg) return LILICORR_ERR_UNSUPPORTED;
   if (plan.lds_bytes > 160 * 1024) return LILICORR_ERR_UNSUPPORTED;
