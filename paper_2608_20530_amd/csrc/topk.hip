@@ -31,6 +31,7 @@
 //    second kernel merges them.
 #include <hip/hip_runtime.h>
 #include <climits>
+#include <type_traits>
 #include <math.h>
 #include <stdint.h>
 
@@ -694,32 +695,246 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
   }
 }
 
+// ---- short row segments --------------------------------------------------------------------
+// Rows split over many workgroups (few rows) leave each workgroup a short segment, where the
+// streaming kernel's fixed costs (producer/consumer set-up, threshold seeding, ring hand-offs)
+// dominate. Segments of at most kSmallSpan logits take this kernel instead and write the same
+// partial record for the merge kernel. Every thread holds 32 logits (element tid + 256 j), all
+// loaded before the first is used. The workgroup reduces the maximum and the exp sum relative to
+// the same integer log2 reference as the streaming kernel.
+// Top-K: each wave finds the K-th largest of its 64 lane maxima by a bitwise search over their
+// order bits (one ballot per bit). At least K of the wave's elements reach it, so the segment's
+// K largest keys all reach the largest of the four waves' values, T. The elements >= T are the
+// candidates (usually little more than K): each lane counts its own, a prefix sum over the wave
+// places them in LDS, and wave 0 ranks them (a key's rank is the number of larger candidates;
+// keys are distinct) and writes the K largest in order. When more than 64 elements reach T
+// (exact ties at T, e.g. a segment that is all -inf), the search is repeated over the lanes'
+// largest keys, ids included (the smallest id wins a tie), which bounds the candidates by key;
+// more than 64 still take a sort-and-merge loop.
+constexpr int kSmallThreads = 256;
+constexpr int kSmallPer = 32;
+constexpr int64_t kSmallSpan = (int64_t)kSmallThreads * kSmallPer;
+constexpr int kSmallFill = 512;  // workgroups that run at once (two per compute unit)
+
+// Exclusive prefix sum over the wave of a per-lane count below 64, from one ballot per bit.
+__device__ __forceinline__ int wave_prefix_small(int c) {
+  int p = 0;
+#pragma unroll
+  for (int bit = 0; bit < 6; ++bit) {
+    const uint64_t bal = __ballot((c >> bit) & 1);
+    p += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u)) << bit;
+  }
+  return p;
+}
+
+// The largest t with at least `need` lanes of the wave holding v >= t among those with `on` set.
+__device__ __forceinline__ uint32_t wave_kth_bits(uint32_t v, bool on, int need) {
+  uint32_t t = 0;
+#pragma unroll
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    if (__popcll(__ballot(on && v >= c)) >= need) t = c;
+  }
+  return t;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(
+    const void* __restrict__ logits, int64_t V, int K, int split,
+    unsigned char* __restrict__ partials) {
+  constexpr int NW = kSmallThreads / kWave;
+  __shared__ uint64_t sCand[kSmallSpan];
+  __shared__ float sMax[NW], sSum[NW];
+  __shared__ uint64_t sT[NW];
+  __shared__ int sCount[2];
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  const int64_t row = blockIdx.x / split;
+  const int part = blockIdx.x % split;
+  const int64_t span = (V + split - 1) / split;
+  const int64_t lo = (int64_t)part * span;
+  const int64_t hi = lo + span < V ? lo + span : V;
+  const int len = (int)(hi > lo ? hi - lo : 0);
+  const int64_t base = row * V + lo;
+  const int rem = len - tid;  // element j of this thread lies in the segment iff 256 j < rem
+  if (tid == 0) sCount[0] = sCount[1] = 0;
+
+  // positions past the segment load the row's first element (in bounds for any segment, even an
+  // empty one) and are masked afterwards, so no load waits behind another
+  float x[kSmallPer];
+  const int64_t rowstart = row * V;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    const int64_t g = kSmallThreads * j < rem ? base + tid + kSmallThreads * j : rowstart;
+    if constexpr (BF16)
+      x[j] = __uint_as_float((uint32_t)static_cast<const uint16_t*>(logits)[g] << 16);
+    else
+      x[j] = static_cast<const float*>(logits)[g];
+  }
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) {
+    x[j] = kSmallThreads * j < rem ? x[j] : -__builtin_inff();
+    m = fmaxf(m, x[j]);
+  }
+  const uint32_t khi = rem > 0 ? order_bits(m) : 0u;  // the lane's largest value (0: none)
+  const uint32_t thi = wave_kth_bits(khi, true, K);
+  const float mw = wave_max(m);
+  if (lane == 0) {
+    sMax[wave] = mw;
+    sT[wave] = thi;
+  }
+  __syncthreads();
+  float M = sMax[0];
+  uint32_t Thi = (uint32_t)sT[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) {
+    M = fmaxf(M, sMax[w]);
+    Thi = (uint32_t)sT[w] > Thi ? (uint32_t)sT[w] : Thi;
+  }
+  const bool valid = M > -__builtin_inff();
+  const int C = valid ? ref_for(M) : 0;
+  const float c = -(float)C;
+  float e = 0.f;
+#pragma unroll
+  for (int j = 0; j < kSmallPer; ++j) e += __builtin_amdgcn_exp2f(fmaf(x[j], kLog2eF, c));
+  e = wave_sum(e);
+  if (lane == 0) sSum[wave] = e;
+
+  // candidates (value, id) >= (Tv, Tlo): value > Tv, or value == Tv and id part >= Tlo (the first
+  // pass takes every id: value >= Tv). The order bits of -0 and +0 are equal, as are the values;
+  // Thi = 0 (fewer than K elements in every wave) makes every element a candidate; the padding
+  // (-inf) is told apart by position when Tv is -inf. Predicates use non-short-circuit operators
+  // so that they compile to mask arithmetic rather than branches.
+  auto place = [&](auto by_id, float Tv, uint32_t Tlo, int slot) {
+    const int lim = Tv == -__builtin_inff() ? rem : kSmallThreads * kSmallPer;
+    auto cand = [&](int j) {
+      const bool in = kSmallThreads * j < lim;
+      if constexpr (decltype(by_id)::value) {
+        const uint32_t idc = 0xFFFFFFFFu - (uint32_t)(lo + tid + kSmallThreads * j);
+        return in & ((x[j] > Tv) | ((x[j] == Tv) & (idc >= Tlo)));
+      } else {
+        return in & (x[j] >= Tv);
+      }
+    };
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallPer; ++j) cnt += cand(j) ? 1 : 0;
+    int off = wave_prefix_small(cnt);
+    const int wtotal = __shfl(off + cnt, kWave - 1, kWave);
+    int at = 0;
+    if (lane == 0) at = atomicAdd(&sCount[slot], wtotal);
+    off += __shfl(at, 0, kWave);
+#pragma unroll
+    for (int j = 0; j < kSmallPer; ++j)
+      if (cand(j)) sCand[off++] = make_key(x[j], (uint32_t)(lo + tid + kSmallThreads * j));
+  };
+  place(std::false_type{}, Thi ? order_value(Thi) : -__builtin_inff(), 0u, 0);
+  __syncthreads();
+  int total = sCount[0];
+  if (total > kWave) {
+    // ties at T: the same search over the lanes' largest keys (the smallest id holding the lane
+    // maximum), the id bits searched among the lanes whose value is the one found
+    int jm = 0;
+#pragma unroll
+    for (int j = kSmallPer - 1; j >= 0; --j) jm = x[j] == m ? j : jm;
+    const uint32_t klo = 0xFFFFFFFFu - (uint32_t)(lo + tid + kSmallThreads * jm);
+    uint32_t tlo = 0;
+    if (thi != 0) {
+      const int need = K - __popcll(__ballot(khi > thi));
+      tlo = wave_kth_bits(klo, khi == thi, need);
+    }
+    // (every wave read sT before the barrier above)
+    if (lane == 0) sT[wave] = ((uint64_t)thi << 32) | tlo;
+    __syncthreads();
+    uint64_t T = sT[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) T = sT[w] > T ? sT[w] : T;
+    const uint32_t h = (uint32_t)(T >> 32);
+    place(std::true_type{}, h ? order_value(h) : -__builtin_inff(), h ? (uint32_t)T : 0u, 1);
+    __syncthreads();
+    total = sCount[1];
+  }
+  if (wave != 0) return;
+  float S = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) S += sSum[w];
+  unsigned char* q = partials + ((size_t)row * split + part) * partial_stride(K);
+  Partial* hdr = reinterpret_cast<Partial*>(q);
+  uint64_t* keys = reinterpret_cast<uint64_t*>(q + sizeof(Partial));
+  if (lane == 0) {
+    hdr->cref = C;
+    hdr->cvalid = valid ? 1 : 0;
+    hdr->s = valid ? S : 0.f;
+    hdr->pad = 0;
+  }
+  if (total <= kWave) {
+    const uint64_t mine = lane < total ? sCand[lane] : 0ull;
+    int rank = 0;
+    for (int i = 0; i < total; ++i) rank += sCand[i] > mine ? 1 : 0;
+    if (lane < total && rank < K) keys[rank] = mine;
+    if (lane >= total && lane < K) keys[lane] = 0ull;
+  } else {
+    uint64_t L = 0ull;
+    for (int b = 0; b < total; b += kWave) {
+      const uint64_t v = b + lane < total ? sCand[b + lane] : 0ull;
+      L = b == 0 ? sort_desc64_u64(v) : merge_desc64(L, sort_desc64_u64(v));
+    }
+    if (lane < K) keys[lane] = L;
+  }
+}
+
 // One workgroup of four waves per row merges the row's `split` (<= 256) partial results: thread
-// p reads partial p's (reference, exp sum) header and the workgroup reduces them; wave w merges
-// the key lists of partials w, w + 4, ..., with eight lists' loads in flight at a time, and wave
-// 0 merges the four results through LDS.
+// p reads partial p's (reference, exp sum) header and the workgroup reduces them. The key lists:
+//  * when the row holds at most kMergeFast entries (split K), every entry is loaded at once
+//    (eight per thread). Partial p* whose K-th key is the largest, T, holds K keys >= T, so the
+//    row's K largest keys all reach T: only entries >= T are candidates (usually little more
+//    than K; when no partial is full, T = 0 and every key is one), compacted into LDS. Wave 0
+//    ranks them (a key's rank is the number of larger candidates; keys are distinct) and places
+//    the K largest in order; more than 64 candidates take a sort-and-merge loop;
+//  * otherwise wave w merges the lists of partials w, w + 4, ..., eight lists' loads in flight
+//    at a time, and wave 0 merges the four results through LDS.
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBatch = 8;
+constexpr int kMergeFast = kMergeThreads * kMergeBatch;
 
 __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
     const unsigned char* __restrict__ partials, int K, int split, int32_t* __restrict__ ids,
     float* __restrict__ logp, float* __restrict__ feat) {
-  __shared__ int sC[kMergeThreads / kWave];
-  __shared__ float sS[kMergeThreads / kWave];
-  __shared__ uint64_t sL[kMergeThreads / kWave][kWave];
+  constexpr int NW = kMergeThreads / kWave;
+  __shared__ int sC[NW];
+  __shared__ float sS[NW];
+  __shared__ uint64_t sL[NW][kWave];
+  __shared__ uint64_t sCand[kMergeFast];
+  __shared__ unsigned long long sT;
+  __shared__ int sCount;
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int64_t row = blockIdx.x;
   const size_t stride = partial_stride(K);
   const unsigned char* base = partials + (size_t)row * split * stride;
+  const int E = split * K;
+  const bool fast = E <= kMergeFast;
+  if (tid == 0) {
+    sT = 0ull;
+    sCount = 0;
+  }
 
-  // reference: the largest valid one (no valid partial: reference 0, sum 0)
-  int cref = 0, valid = 0;
-  float s = 0.f;
-  if (tid < split) {
-    const Partial* hdr = reinterpret_cast<const Partial*>(base + (size_t)tid * stride);
-    valid = hdr->cvalid;
-    cref = hdr->cref;
-    s = hdr->s;
+  // reference: the largest valid one (no valid partial: reference 0, sum 0). Every load below is
+  // issued unconditionally (threads past the end read partial 0 or entry 0 and discard it), so
+  // none waits behind another.
+  const Partial* hdr = reinterpret_cast<const Partial*>(base + (size_t)(tid < split ? tid : 0) * stride);
+  int cref = hdr->cref, valid = hdr->cvalid;
+  float s = hdr->s;
+  if (tid >= split) valid = 0;
+  // entries tid + 256 i of the row (fast path)
+  uint64_t kv[kMergeBatch];
+  if (fast) {
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const int e = tid + kMergeThreads * i < E ? tid + kMergeThreads * i : 0;
+      kv[i] = reinterpret_cast<const uint64_t*>(base + (size_t)(e / K) * stride +
+                                                sizeof(Partial))[e % K];
+    }
   }
   int c = valid ? cref : INT_MIN;
 #pragma unroll
@@ -731,26 +946,74 @@ __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
   __syncthreads();
   int C = sC[0];
 #pragma unroll
-  for (int w = 1; w < kMergeThreads / kWave; ++w) C = sC[w] > C ? sC[w] : C;
+  for (int w = 1; w < NW; ++w) C = sC[w] > C ? sC[w] : C;
   if (C == INT_MIN) C = 0;
   float part = valid ? ldexpf(s, cref - C) : 0.f;
   part = wave_sum(part);
   if (lane == 0) sS[wave] = part;
 
   uint64_t merged = 0;
+  if (fast) {
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const int e = tid + kMergeThreads * i;
+      if (e < E && e % K == K - 1) atomicMax(&sT, (unsigned long long)kv[i]);
+    }
+    __syncthreads();
+    const uint64_t T = sT;
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const bool q = tid + kMergeThreads * i < E && kv[i] != 0ull && kv[i] >= T;
+      cnt += q ? 1 : 0;
+    }
+    int off = wave_prefix_small(cnt);
+    const int wtotal = __shfl(off + cnt, kWave - 1, kWave);
+    int at = 0;
+    if (lane == 0) at = atomicAdd(&sCount, wtotal);
+    off += __shfl(at, 0, kWave);
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i)
+      if (tid + kMergeThreads * i < E && kv[i] != 0ull && kv[i] >= T) sCand[off++] = kv[i];
+    __syncthreads();
+    if (wave != 0) return;
+    const int total = sCount;
+    if (total <= kWave) {
+      const uint64_t mine = lane < total ? sCand[lane] : 0ull;
+      int rank = 0;
+      for (int i = 0; i < total; ++i) rank += sCand[i] > mine ? 1 : 0;
+      if (lane < total && rank < K) sL[0][rank] = mine;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      merged = lane < K ? sL[0][lane] : 0ull;
+    } else {
+      for (int b = 0; b < total; b += kWave) {
+        const uint64_t v = b + lane < total ? sCand[b + lane] : 0ull;
+        merged = b == 0 ? sort_desc64_u64(v) : merge_desc64(merged, sort_desc64_u64(v));
+      }
+    }
+    float S = sS[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) S += sS[w];
+    write_row(merged, (log2((double)S) + (double)C) / (double)kLog2eF, row, K, ids, logp, feat);
+    return;
+  }
+
   bool first = true;
-  for (int p0 = wave; p0 < split; p0 += kMergeBatch * (kMergeThreads / kWave)) {
+  for (int p0 = wave; p0 < split; p0 += kMergeBatch * NW) {
     uint64_t k[kMergeBatch];
 #pragma unroll
     for (int b = 0; b < kMergeBatch; ++b) {
-      const int p = p0 + b * (kMergeThreads / kWave);
-      k[b] = 0ull;
-      if (p < split && lane < K)
-        k[b] = reinterpret_cast<const uint64_t*>(base + (size_t)p * stride + sizeof(Partial))[lane];
+      const int p = p0 + b * NW;
+      k[b] = reinterpret_cast<const uint64_t*>(base + (size_t)(p < split ? p : 0) * stride +
+                                               sizeof(Partial))[lane < K ? lane : 0];
     }
 #pragma unroll
+    for (int b = 0; b < kMergeBatch; ++b) k[b] = (p0 + b * NW < split && lane < K) ? k[b] : 0ull;
+#pragma unroll
     for (int b = 0; b < kMergeBatch; ++b) {
-      const int p = p0 + b * (kMergeThreads / kWave);
+      const int p = p0 + b * NW;
       if (p < split) {
         merged = first ? k[b] : merge_desc64(merged, k[b]);
         first = false;
@@ -762,7 +1025,7 @@ __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
   if (wave == 0) {
     float S = sS[0];
 #pragma unroll
-    for (int w = 1; w < kMergeThreads / kWave; ++w) {
+    for (int w = 1; w < NW; ++w) {
       S += sS[w];
       merged = merge_desc64(merged, sL[w][lane]);
     }
@@ -778,6 +1041,12 @@ int topk_split(int64_t rows, int64_t V, bool bf16) {
   int64_t by_fill = (target + rows - 1) / rows;
   int64_t by_len = V / (2 * wg_tile);
   int64_t s = by_fill < by_len ? by_fill : by_len;
+  if (s < by_fill) {
+    // too few rows to fill the chip with streaming segments: when every row's short segments (at
+    // most kSmallSpan logits) run at once, they take the short-segment kernel
+    const int64_t t = (V + kSmallSpan - 1) / kSmallSpan;
+    if (t > 1 && t <= 256 && rows * t <= kSmallFill) s = t;
+  }
   if (s < 1) s = 1;
   if (s > 256) s = 256;
   (void)bf16;
@@ -823,7 +1092,14 @@ static lilicorr_status topk_launch(const void* logits, lilicorr_dtype dtype, int
 
   dim3 grid((unsigned)(rows * split)), block(kTopkWaves * kWave);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  if (bf16)
+  const bool small = split > 1 && (V + split - 1) / split <= kSmallSpan;
+  if (small && bf16)
+    hipLaunchKernelGGL(topk_small_kernel<true>, grid, dim3(kSmallThreads), 0, stream, logits, V, K,
+                       split, ws);
+  else if (small)
+    hipLaunchKernelGGL(topk_small_kernel<false>, grid, dim3(kSmallThreads), 0, stream, logits, V,
+                       K, split, ws);
+  else if (bf16)
     hipLaunchKernelGGL(topk_lse_kernel<true>, grid, block, 0, stream, logits, V, K, split, ids, logp,
                        feat, ws);
   else

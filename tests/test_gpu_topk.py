@@ -71,8 +71,18 @@ EDGE = [
     (1, 2, 5000, 8, "equal"),
     (1, 2, 3000, 20, "zeros"),
     (2, 2, 4099, 10, "neginf"),
-    (1, 16, 151936, 8, "normal"),  # few rows: split over many workgroups + merge kernel
+    (1, 16, 151936, 8, "normal"),  # few rows: short segments of 8192 + merge kernel
     (1, 1, 262144, 64, "ties"),
+    # short segments with exact ties at the threshold (lane maxima all equal: the id search)
+    (1, 2, 20000, 8, "equal"),
+    (1, 2, 20000, 20, "zeros"),
+    (2, 2, 20001, 10, "neginf"),
+    (1, 3, 30000, 12, "maskblock"),  # whole segments at -inf next to finite ones
+    (1, 1, 20000, 64, "ties"),
+    # a split that leaves rows*segments above one round: streaming segments + merge
+    (2, 16, 151936, 16, "normal"),
+    # more than 2048 partial keys per row: the merge kernel's list-merging path
+    (1, 1, 300000, 64, "normal"),
 ]
 
 
@@ -86,6 +96,10 @@ def _edge_logits(N, B, V, kind, seed):
         x = np.full((N, B, V), 1.5)
     elif kind == "zeros":
         x = rng.choice([-0.0, 0.0, -1.0], size=(N, B, V))
+    elif kind == "maskblock":
+        x = rng.standard_normal((N, B, V))
+        x[..., : V // 2] = -np.inf
+        x[..., -1] = 3.0
     elif kind == "neginf":
         x = rng.standard_normal((N, B, V))
         x[rng.random((N, B, V)) < 0.9] = -np.inf
