@@ -445,6 +445,36 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_dma_kernel(GemmArgs p) {
   // four consecutive rows of one request when L % 4 == 0 (a block's rows start at a multiple of
   // 4): one 8-byte store per column into V^T
   const bool vfast = vpart && (p.L % 4 == 0);
+  if constexpr (MODE == kModeResid) {
+    // X += acc: the 32 values of 16-row block mt + 1 are loaded (rows past M clamped to the last
+    // row and not stored) before block mt is added and stored, so the loads of consecutive
+    // blocks overlap instead of each block waiting on its own
+    float xv[2][4][8];
+    auto load = [&](int mt, float (&d)[4][8]) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        int64_t row = rbase + mt * 16 + j;
+        row = row < p.M ? row : p.M - 1;
+#pragma unroll
+        for (int nt2 = 0; nt2 < 8; ++nt2) d[j][nt2] = p.X[row * p.N + cbase + nt2 * 16];
+      }
+    };
+    load(0, xv[0]);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      if (mt + 1 < 4) load(mt + 1, xv[(mt + 1) & 1]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t row = rbase + mt * 16 + j;
+        if (row < p.M) {
+#pragma unroll
+          for (int nt2 = 0; nt2 < 8; ++nt2)
+            p.X[row * p.N + cbase + nt2 * 16] = xv[mt & 1][j][nt2] + acc[mt][nt2][j];
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
     const int64_t row0 = rbase + mt * 16;

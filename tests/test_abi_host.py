@@ -62,6 +62,17 @@ def test_size_queries(L):
     # a single request is split over several workgroups per row
     assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) > 0
     assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 65) == 0
+    # the split rule, through the workspace size (rows x segments x (16-byte header + K keys)):
+    # few rows whose short segments (<= 8192 logits) all run at once take ceil(V / 8192) of them
+    part = lambda K: 16 + 8 * K
+    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) == 16 * 19 * part(8)
+    assert L.lilicorr_topk_workspace_bytes(1, 8, 32000, 4) == 8 * 4 * part(4)
+    assert L.lilicorr_topk_workspace_bytes(1, 1, 300000, 64) == 37 * part(64)
+    # more rows x segments than run at once: streaming segments of >= 12288 logits
+    assert L.lilicorr_topk_workspace_bytes(2, 16, 151936, 16) == 32 * 12 * part(16)
+    assert L.lilicorr_topk_workspace_bytes(16, 16, 151936, 16) == 256 * 4 * part(16)
+    # rows shorter than one short segment stay whole
+    assert L.lilicorr_topk_workspace_bytes(1, 2, 5000, 8) == 0
 
 
 A = 4096  # a fake, 16-byte aligned "device" address: never dereferenced on these paths
