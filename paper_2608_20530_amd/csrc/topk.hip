@@ -702,19 +702,22 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
 // partial record for the merge kernel. Every thread holds 32 logits (element tid + 256 j), all
 // loaded before the first is used. The workgroup reduces the maximum and the exp sum relative to
 // the same integer log2 reference as the streaming kernel.
-// Top-K: each wave finds the K-th largest of its 64 lane maxima by a bitwise search over their
-// order bits (one ballot per bit). At least K of the wave's elements reach it, so the segment's
-// K largest keys all reach the largest of the four waves' values, T. The elements >= T are the
-// candidates (usually little more than K): each lane counts its own, a prefix sum over the wave
-// places them in LDS, and wave 0 ranks them (a key's rank is the number of larger candidates;
-// keys are distinct) and writes the K largest in order. When more than 64 elements reach T
-// (exact ties at T, e.g. a segment that is all -inf), the search is repeated over the lanes'
-// largest keys, ids included (the smallest id wins a tie), which bounds the candidates by key;
-// more than 64 still take a sort-and-merge loop.
+// Top-K: a threshold T that at least K of the segment's elements reach, so that its K largest
+// keys all do. At K <= 8 each wave finds the K-th largest of its 64 lane maxima by a bitwise
+// search over their order bits (one ballot per bit) and T is the largest of the four; at larger K
+// (where that leaves more than 64 candidates on random logits) T is the K-th largest of all 256
+// lane maxima (every wave reads them from LDS; four ballots per bit). The elements >= T are the
+// candidates: each lane counts its own, a prefix sum over the wave places them in LDS, and wave 0
+// ranks them (a key's rank is the number of larger candidates; keys are distinct) and writes the
+// K largest in order. When more than 64 elements reach T (exact ties at T, such as a segment that
+// is all -inf), T becomes the workgroup-wide value completed over the ids of the lane maxima (the
+// smallest id holding each) where more lanes than needed hold it, which bounds the candidates by
+// key; more than 64 still take a sort-and-merge loop.
 constexpr int kSmallThreads = 256;
 constexpr int kSmallPer = 32;
 constexpr int64_t kSmallSpan = (int64_t)kSmallThreads * kSmallPer;
 constexpr int kSmallFill = 512;  // workgroups that run at once (two per compute unit)
+constexpr int kSmallWaveK = 8;   // largest K whose first threshold is taken per wave
 
 // Exclusive prefix sum over the wave of a per-lane count below 64, from one ballot per bit.
 __device__ __forceinline__ int wave_prefix_small(int c) {
@@ -728,13 +731,29 @@ __device__ __forceinline__ int wave_prefix_small(int c) {
   return p;
 }
 
-// The largest t with at least `need` lanes of the wave holding v >= t among those with `on` set.
-__device__ __forceinline__ uint32_t wave_kth_bits(uint32_t v, bool on, int need) {
+// The largest t with at least `need` lanes of the wave holding v >= t.
+__device__ __forceinline__ uint32_t wave_kth_bits(uint32_t v, int need) {
   uint32_t t = 0;
 #pragma unroll
   for (int bit = 31; bit >= 0; --bit) {
     const uint32_t c = t | (1u << bit);
-    if (__popcll(__ballot(on && v >= c)) >= need) t = c;
+    if (__popcll(__ballot(v >= c)) >= need) t = c;
+  }
+  return t;
+}
+
+// The largest t such that at least `need` of the workgroup's 256 values v[] (four per lane of
+// every wave, read from LDS, so every wave finds the same t) with on[] set are >= t.
+__device__ __forceinline__ uint32_t block_kth_bits(const uint32_t (&v)[4], const bool (&on)[4],
+                                                   int need) {
+  uint32_t t = 0;
+#pragma unroll
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    int n = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) n += __popcll(__ballot(on[i] & (v[i] >= c)));
+    if (n >= need) t = c;
   }
   return t;
 }
@@ -746,7 +765,7 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(
   constexpr int NW = kSmallThreads / kWave;
   __shared__ uint64_t sCand[kSmallSpan];
   __shared__ float sMax[NW], sSum[NW];
-  __shared__ uint64_t sT[NW];
+  __shared__ uint32_t sKhi[kSmallThreads], sKlo[kSmallThreads];
   __shared__ int sCount[2];
   const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
   const int64_t row = blockIdx.x / split;
@@ -778,20 +797,29 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(
     m = fmaxf(m, x[j]);
   }
   const uint32_t khi = rem > 0 ? order_bits(m) : 0u;  // the lane's largest value (0: none)
-  const uint32_t thi = wave_kth_bits(khi, true, K);
+  // the threshold: at K <= 8 the largest of the waves' K-th lane maxima (about 4K candidates),
+  // else the K-th largest of all 256 lane maxima (a tighter bound for a costlier search)
+  const bool per_wave = K <= kSmallWaveK;
+  sKhi[tid] = khi;
+  const uint32_t thi = per_wave ? wave_kth_bits(khi, K) : 0u;
   const float mw = wave_max(m);
   if (lane == 0) {
     sMax[wave] = mw;
-    sT[wave] = thi;
+    sKlo[wave] = thi;  // the waves' thresholds (sKlo is reused for lane ids only later)
   }
   __syncthreads();
   float M = sMax[0];
-  uint32_t Thi = (uint32_t)sT[0];
+  uint32_t Thi = sKlo[0];
 #pragma unroll
   for (int w = 1; w < NW; ++w) {
     M = fmaxf(M, sMax[w]);
-    Thi = (uint32_t)sT[w] > Thi ? (uint32_t)sT[w] : Thi;
+    Thi = sKlo[w] > Thi ? sKlo[w] : Thi;
   }
+  uint32_t all_hi[4];
+  const bool every[4] = {true, true, true, true};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) all_hi[i] = sKhi[lane + kWave * i];
+  if (!per_wave) Thi = block_kth_bits(all_hi, every, K);
   const bool valid = M > -__builtin_inff();
   const int C = valid ? ref_for(M) : 0;
   const float c = -(float)C;
@@ -833,25 +861,28 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(
   __syncthreads();
   int total = sCount[0];
   if (total > kWave) {
-    // ties at T: the same search over the lanes' largest keys (the smallest id holding the lane
-    // maximum), the id bits searched among the lanes whose value is the one found
+    // the K-th largest of all 256 lane maxima, then, among the lanes holding exactly that value,
+    // the id bits of their keys (the smallest id holding the lane maximum)
+    if (per_wave) Thi = block_kth_bits(all_hi, every, K);
     int jm = 0;
 #pragma unroll
     for (int j = kSmallPer - 1; j >= 0; --j) jm = x[j] == m ? j : jm;
-    const uint32_t klo = 0xFFFFFFFFu - (uint32_t)(lo + tid + kSmallThreads * jm);
-    uint32_t tlo = 0;
-    if (thi != 0) {
-      const int need = K - __popcll(__ballot(khi > thi));
-      tlo = wave_kth_bits(klo, khi == thi, need);
-    }
-    // (every wave read sT before the barrier above)
-    if (lane == 0) sT[wave] = ((uint64_t)thi << 32) | tlo;
+    sKlo[tid] = 0xFFFFFFFFu - (uint32_t)(lo + tid + kSmallThreads * jm);  // every wave read sKlo[w]
     __syncthreads();
-    uint64_t T = sT[0];
+    uint32_t Tlo = 0;
+    if (Thi != 0) {
+      uint32_t all_lo[4];
+      bool at_t[4];
+      int above = 0;
 #pragma unroll
-    for (int w = 1; w < NW; ++w) T = sT[w] > T ? sT[w] : T;
-    const uint32_t h = (uint32_t)(T >> 32);
-    place(std::true_type{}, h ? order_value(h) : -__builtin_inff(), h ? (uint32_t)T : 0u, 1);
+      for (int i = 0; i < 4; ++i) {
+        all_lo[i] = sKlo[lane + kWave * i];
+        at_t[i] = all_hi[i] == Thi;
+        above += __popcll(__ballot(all_hi[i] > Thi));
+      }
+      Tlo = block_kth_bits(all_lo, at_t, K - above);
+    }
+    place(std::true_type{}, Thi ? order_value(Thi) : -__builtin_inff(), Tlo, 1);
     __syncthreads();
     total = sCount[1];
   }
