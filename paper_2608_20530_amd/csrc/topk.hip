@@ -831,8 +831,9 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small_kernel(
 
   // candidates (value, id) >= (Tv, Tlo): value > Tv, or value == Tv and id part >= Tlo (the first
   // pass takes every id: value >= Tv). The order bits of -0 and +0 are equal, as are the values;
-  // Thi = 0 (fewer than K elements in every wave) makes every element a candidate; the padding
-  // (-inf) is told apart by position when Tv is -inf. Predicates use non-short-circuit operators
+  // Thi = 0 (fewer than K lanes holding elements, in every wave or in the workgroup, as searched)
+  // makes every element a candidate; the padding (-inf) is told apart by position when Tv is
+  // -inf. Predicates use non-short-circuit operators
   // so that they compile to mask arithmetic rather than branches.
   auto place = [&](auto by_id, float Tv, uint32_t Tlo, int slot) {
     const int lim = Tv == -__builtin_inff() ? rem : kSmallThreads * kSmallPer;
