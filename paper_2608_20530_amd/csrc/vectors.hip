@@ -158,6 +158,8 @@ __global__ __launch_bounds__(kF32Threads) void cand_vectors_f32_kernel(
 #pragma unroll
     for (int r = 0; r < kF32Rows; ++r) u[q][r] = 0.f;
     if (j < d) {
+      // unrolled so that several weight loads are in flight at once (d is a multiple of 16)
+#pragma unroll 16
       for (int i = 0; i < d; ++i) {
         const float w = W[(int64_t)i * d + j];
 #pragma unroll
