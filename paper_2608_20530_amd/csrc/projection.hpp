@@ -35,9 +35,11 @@ struct VecGeom {
   int rm;     // 16-row blocks per workgroup of the candidate-vector kernel
 };
 
-// rm: up to d = 512, 128-row tiles once there are enough of them to give every compute unit
+// rm: up to d = 256, 128-row tiles once there are enough of them to give every compute unit
 // several (a workgroup's phases, gather -> MFMA -> store, then overlap with other workgroups'),
-// else 64-row tiles, which put two workgroups on each compute unit; 32-row tiles above d = 512
+// else 64-row tiles, which put two workgroups on each compute unit; 64-row tiles for
+// 256 < d <= 512 (a 128-row tile there needs 133 KB of LDS, one workgroup per compute unit, and
+// measured 7% slower at 131072 rows, d = 512); 32-row tiles above d = 512
 inline VecGeom vec_geom(int d, int64_t M = 0) {
   VecGeom g;
   g.d16 = d / 16;
@@ -45,7 +47,7 @@ inline VecGeom vec_geom(int d, int64_t M = 0) {
   g.dk = (d + 31) / 32;
   g.dkp = (g.dk + 1) / 2 * 2;
   g.waves = g.nbp / kNbPerWave;
-  g.rm = d > 512 ? 2 : ((M + 127) / 128 * 2 >= 2048 ? 8 : 4);
+  g.rm = d > 512 ? 2 : (d > 256 ? 4 : ((M + 127) / 128 * 2 >= 2048 ? 8 : 4));
   return g;
 }
 
