@@ -50,6 +50,8 @@ typedef enum {
     LILICORR_ERR_ALIGNMENT = -3,   /* a pointer is not 16-byte aligned */
     LILICORR_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
     LILICORR_ERR_HIP = -5,         /* a kernel launch failed */
+    LILICORR_ERR_TIMEOUT = -6,     /* a bounded wait inside a kernel gave up (see
+                                      lilicorr_topk_wait_status): outputs are invalid */
 } lilicorr_status;
 
 /*
@@ -61,14 +63,37 @@ typedef enum {
  *   logits    [N][B][V] in `dtype` (LILICORR_F32 or LILICORR_BF16), read once.
  *   ids       [N][B][K] int32 out: token ids ordered by logit descending, ties to the lower id
  *             (-0 and +0 compare equal).
- *   logp      [N][B][K] fp32 out: logits[id] - log(sum_v exp(logits[v])).
- *   workspace device scratch of at least lilicorr_topk_workspace_bytes(N, B, V, K) bytes (may be
- *             NULL when that is 0); owned by the caller, no initial contents needed, clobbered.
+ *   logp      [N][B][K] fp32 out: logits[id] - log(sum_v exp(logits[v])). The same inputs give
+ *             the same ids and logp bit for bit on every call.
+ *   workspace device scratch of at least lilicorr_topk_workspace_bytes(N, B, V, K) bytes (at
+ *             least 256), owned by the caller and zero-filled once before its first use. Its
+ *             first 256 bytes hold the wait status word (below), which the calls only ever set;
+ *             the rest is clobbered by every call. Calls sharing a workspace must not overlap.
+ *
+ * The kernel's waits (a producer wave for ring space, the consumer wave for work) are bounded.
+ * A wait that gives up (never expected: the bound is ~4M polls) does not stop the kernel: the
+ * call completes, its outputs are invalid, and a bit is set in the workspace's status word.
  */
 size_t lilicorr_topk_workspace_bytes(int64_t N, int64_t B, int64_t V, int K);
 lilicorr_status lilicorr_topk(const void *logits, lilicorr_dtype dtype, int64_t N, int64_t B,
                               int64_t V, int K, int32_t *ids, float *logp, void *workspace,
                               size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Wait status of the top-K calls that used `workspace` since its status word was last cleared:
+ * waits for `stream` to finish what it holds, reads the word, clears it, and returns
+ * LILICORR_ERR_TIMEOUT if some wait gave up (the outputs of at least one of those calls are
+ * invalid), LILICORR_OK otherwise. Synchronous; not for use inside graph capture.
+ * LILICORR_ERR_INVALID_ARG for a NULL workspace, LILICORR_ERR_HIP if a HIP call fails.
+ */
+lilicorr_status lilicorr_topk_wait_status(const void *workspace, hipStream_t stream);
+
+/*
+ * Spin limit of the bounded waits in kernels launched after this call, process-wide (a testing
+ * and diagnosis hook: a small limit makes waits give up so that their reporting can be checked
+ * while every kernel still runs to its end). spins < 0 restores the default (2^22).
+ */
+void lilicorr_set_wait_limit(int64_t spins);
 
 /*
  * Step 1 with the candidates' confidence features: the same call as lilicorr_topk (same
@@ -151,12 +176,14 @@ lilicorr_status lilicorr_greedy_walk(const float *S, const float *S0, const floa
  * (+ logp_weight * sum_t logp[n][t][c_t]), with P_0 = S0[n] or all zero when S0 is NULL, found
  * by dynamic programming in O(B K^2). Ties go to the lowest index (predecessor and final
  * candidate), which returns, among all maximising paths, the smallest read from the last slot
- * backwards. Sums and comparisons are fp32 with one rounding per addition.
+ * backwards. Path sums and comparisons are double: every fp32 term is widened exactly and each
+ * partial sum is rounded once, in the order of g above (the lambda term after its slot's matching
+ * term), so the maximiser is exact unless two path sums differ by less than that rounding.
  *   S, S0, logp, ids, logp_weight   as for lilicorr_greedy_walk.
  *   draft, choice  [N][B] int32 out (choice may be NULL): the path's tokens and indices.
  *   logq           [N][B] fp32 out or NULL: Eq. (localar) along the path,
  *                  z_t[c_t] - log sum_k exp z_t[k] with z_t[k] = P_t(c_{t-1}, k) (+ lambda logp).
- *   score          [N] fp32 out or NULL: g of the returned path.
+ *   score          [N] fp32 out or NULL: g of the returned path, rounded once to fp32.
  * Limits: K <= 64, B <= 8192, B * K <= 65536 (LILICORR_ERR_UNSUPPORTED otherwise).
  */
 lilicorr_status lilicorr_viterbi_walk(const float *S, const float *S0, const float *logp,

@@ -272,10 +272,14 @@ int oracle_greedy_walk(const float *S, const float *S0, const float *logp, const
  * candidate of the last slot. Ties go to the lowest index, for predecessors and for the final
  * candidate: among all maximising paths this returns the one that is smallest when read from the
  * last slot backwards.
- * The sums and comparisons run in float, one rounding per addition (and one fmaf for the lambda
- * term): the precision the GPU kernel decides in, so both sides take the same decisions.
- * logq[t] is Eq. (localar) along the returned path, z_t[k] = P_t(c_{t-1}, k) (+ lambda logp),
- * logq[t] = z_t[c_t] - log sum_k exp z_t[k], in double from the float z; score[n] = g (float).
+ * Path sums and comparisons are in double: each float term is widened exactly and every partial
+ * sum is rounded once, in the order of the sum above (the lambda term, an exact product of two
+ * floats in double, is added after the matching term of its slot). The maximiser is therefore the
+ * exact one unless two path sums differ by less than the double rounding of the partial sums
+ * (about B * 2^-53 * max |partial sum|).
+ * logq[t] is Eq. (localar) along the returned path, z_t[k] = P_t(c_{t-1}, k) (+ lambda logp), the
+ * node score of the greedy walk, logq[t] = z_t[c_t] - log sum_k exp z_t[k], in double from the
+ * float z; score[n] = g of the returned path, rounded once to float.
  * ------------------------------------------------------------------------------------------- */
 
 int oracle_viterbi_walk(const float *S, const float *S0, const float *logp, const int32_t *ids,
@@ -286,43 +290,44 @@ int oracle_viterbi_walk(const float *S, const float *S0, const float *logp, cons
         return -1;
     if (B > 1 && !S)
         return -1;
-    float *best = (float *)malloc(sizeof(float) * (size_t)K);
-    float *next = (float *)malloc(sizeof(float) * (size_t)K);
+    const double lam = (double)logp_weight;
+    double *best = (double *)malloc(sizeof(double) * (size_t)K);
+    double *next = (double *)malloc(sizeof(double) * (size_t)K);
     float *z = (float *)malloc(sizeof(float) * (size_t)K);
     int *from = (int *)malloc(sizeof(int) * (size_t)(B * K));
     int *path = (int *)malloc(sizeof(int) * (size_t)B);
     for (int64_t n = 0; n < N; ++n) {
         for (int k = 0; k < K; ++k) {
-            float v = S0 ? S0[n * K + k] : 0.0f;
+            double v = S0 ? (double)S0[n * K + k] : 0.0;
             if (logp_weight != 0.0f)
-                v = fmaf(logp_weight, logp[(n * B + 0) * K + k], v);
+                v += lam * (double)logp[(n * B + 0) * K + k];
             best[k] = v;
         }
         for (int64_t t = 1; t < B; ++t) {
             const float *St = S + (n * (B - 1) + (t - 1)) * K * (int64_t)K;
             for (int k = 0; k < K; ++k) {
-                float bv = best[0] + St[0 * K + k];
+                double bv = best[0] + (double)St[0 * K + k];
                 int bp = 0;
                 for (int p = 1; p < K; ++p) {
-                    const float v = best[p] + St[p * K + k];
+                    const double v = best[p] + (double)St[p * K + k];
                     if (v > bv) {
                         bv = v;
                         bp = p;
                     }
                 }
                 if (logp_weight != 0.0f)
-                    bv = fmaf(logp_weight, logp[(n * B + t) * K + k], bv);
+                    bv += lam * (double)logp[(n * B + t) * K + k];
                 next[k] = bv;
                 from[t * K + k] = bp;
             }
-            memcpy(best, next, sizeof(float) * (size_t)K);
+            memcpy(best, next, sizeof(double) * (size_t)K);
         }
         int c = 0;
         for (int k = 1; k < K; ++k)
             if (best[k] > best[c])
                 c = k;
         if (score)
-            score[n] = best[c];
+            score[n] = (float)best[c];
         path[B - 1] = c;
         for (int64_t t = B - 1; t >= 1; --t)
             path[t - 1] = from[t * K + path[t]];

@@ -4,6 +4,7 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
 
   lilicorr_topk               logits [N,B,V] -> ids, logp [N,B,K]       (Sec. 3.2; serving appendix)
   lilicorr_topk_features      ... plus the five confidence scalars      (implementation appendix)
+  lilicorr_topk_wait_status   reads and clears a top-K workspace's wait status word
   lilicorr_pack_weights       W_in, W_out [d,d] -> matrix-core layout   (once per weight set)
   lilicorr_candidate_vectors  ids, E -> in_vec, out_vec [N,B,K,d]       (Sec. 3.2 unit-norm heads)
   lilicorr_pair_scores        in/out -> S [N,B-1,K,K] (+ S0 [N,K])      (Eq. pair)
@@ -28,14 +29,15 @@ import torch
 
 __all__ = [
     "LIB_PATH", "load_library", "LilicorrError", "SIGMA",
-    "lilicorr_topk", "lilicorr_topk_features", "lilicorr_topk_workspace_bytes", "lilicorr_packed_weight_bytes",
+    "lilicorr_topk", "lilicorr_topk_features", "lilicorr_topk_workspace_bytes",
+    "lilicorr_topk_wait_status", "lilicorr_set_wait_limit", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
     "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
     "lilicorr_score_walk_certified", "lilicorr_score_walk_certified_workspace_bytes",
     "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes",
     "lilicorr_block_graph_create", "lilicorr_block_graph_launch", "lilicorr_block_graph_destroy",
     "BlockArgs", "BlockGraph", "lilicorr_status_string",
-    "topk", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk", "score_viterbi",
+    "topk", "topk_workspace", "topk_wait_status", "pack_weights", "candidate_vectors", "pair_scores", "greedy_walk", "viterbi_walk", "score_walk", "score_viterbi",
     "score_walk_certified", "score_walk_certified_workspace", "CERT_MARGIN", "draft_block",
     "ScorerLayer", "lilicorr_scorer_packed_bytes", "lilicorr_scorer_pack",
     "lilicorr_scorer_workspace_bytes", "lilicorr_scorer_forward", "scorer_pack", "scorer_workspace",
@@ -96,6 +98,8 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_topk_workspace_bytes": ([I64, I64, I64, I], SZ),
         "lilicorr_topk": ([P, I, I64, I64, I64, I, P, P, P, SZ, P], I),
         "lilicorr_topk_features": ([P, I, I64, I64, I64, I, P, P, P, P, SZ, P], I),
+        "lilicorr_topk_wait_status": ([P, P], I),
+        "lilicorr_set_wait_limit": ([I64], None),
         "lilicorr_packed_weight_bytes": ([I], SZ),
         "lilicorr_pack_weights": ([P, P, I, P, P], I),
         "lilicorr_candidate_vectors": ([P, P, I, I64, I, P, I64, I64, I, P, P, P], I),
@@ -143,6 +147,19 @@ def _call(name: str, *args) -> int:
 
 def lilicorr_topk_workspace_bytes(N: int, B: int, V: int, K: int) -> int:
     return int(load_library().lilicorr_topk_workspace_bytes(N, B, V, K))
+
+
+def lilicorr_topk_wait_status(workspace, stream) -> int:
+    """Returns the status (0, or LILICORR_ERR_TIMEOUT = -6 when a wait gave up); raises only when
+    the query itself fails."""
+    rc = load_library().lilicorr_topk_wait_status(workspace, stream)
+    if rc not in (0, -6):
+        raise LilicorrError(f"lilicorr_topk_wait_status: {lilicorr_status_string(rc)} (status {rc})")
+    return rc
+
+
+def lilicorr_set_wait_limit(spins: int) -> None:
+    load_library().lilicorr_set_wait_limit(spins)
 
 
 def lilicorr_packed_weight_bytes(d: int) -> int:
@@ -257,6 +274,20 @@ def _dtype_code(t: torch.Tensor) -> int:
     return BF16 if t.dtype == torch.bfloat16 else F32
 
 
+def topk_workspace(N: int, B: int, V: int, K: int, device="cuda") -> torch.Tensor:
+    """A zero-filled top-K workspace (its status word must start at zero)."""
+    need = lilicorr_topk_workspace_bytes(N, B, V, K)
+    if need == 0:
+        raise LilicorrError(f"topk does not support N={N}, B={B}, V={V}, K={K}")
+    return torch.zeros(need, dtype=torch.uint8, device=device)
+
+
+def topk_wait_status(workspace: torch.Tensor) -> int:
+    """0 if every bounded wait of the top-K calls on `workspace` finished, -6
+    (LILICORR_ERR_TIMEOUT) if one gave up; clears the word. Waits for the current stream."""
+    return lilicorr_topk_wait_status(_dev(workspace, "workspace"), _stream())
+
+
 def topk(logits: torch.Tensor, K: int, *, out=None, workspace=None, features: bool = False):
     """logits [N,B,V] bf16/fp32 -> (ids [N,B,K] int32, logp [N,B,K] fp32[, feat [N,B,K,5] fp32
     when features=True])."""
@@ -268,9 +299,8 @@ def topk(logits: torch.Tensor, K: int, *, out=None, workspace=None, features: bo
         if features:
             out = out + (torch.empty(N, B, K, 5, dtype=torch.float32, device=dev),)
     ids, logp = out[0], out[1]
-    need = lilicorr_topk_workspace_bytes(N, B, V, K)
-    if workspace is None or workspace.numel() < need:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    if workspace is None:
+        workspace = topk_workspace(N, B, V, K, dev)
     args = (_dev(logits, "logits", (torch.bfloat16, torch.float32)), _dtype_code(logits), N, B, V,
             K, _dev(ids, "ids", (torch.int32,)), _dev(logp, "logp", (torch.float32,)))
     if features:
@@ -508,8 +538,7 @@ class BlockGraph:
         self.logits, self.E, self.packed, self.anchor_out = logits, E, packed, anchor_out
         self.ids = torch.empty(N, B, K, dtype=torch.int32, device=dev)
         self.logp = torch.empty(N, B, K, dtype=torch.float32, device=dev)
-        need = lilicorr_topk_workspace_bytes(N, B, V, K)
-        self.topk_workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+        self.topk_workspace = topk_workspace(N, B, V, K, dev)
         self.draft = torch.empty(N, B, dtype=torch.int32, device=dev)
         self.choice = torch.empty(N, B, dtype=torch.int32, device=dev)
         self.logq = torch.empty(N, B, dtype=torch.float32, device=dev)

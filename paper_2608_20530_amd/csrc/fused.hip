@@ -85,7 +85,7 @@ inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = fal
     const int G = K <= 16 ? 16 : (K <= 32 ? 32 : 64);
     const size_t s_bytes = (size_t)(B - 1) * K * (G + 4) * 4;  // transposed, padded to G + 4
     p.stage = s_bytes <= kExactStageBytes;
-    t_bytes = 64 * 4 + (p.stage ? s_bytes : 0) + (size_t)(B * K + B);
+    t_bytes = 64 * 8 + (p.stage ? s_bytes : 0) + (size_t)(B * K + B);
   } else {
     p.rows = 1 + (B - 1) * K;
     p.stage = false;
@@ -367,8 +367,8 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   if (EXACT) {
     const float* xn = xs + n * plan.rows;
     const int64_t nS = (B - 1) * (int64_t)K * K;
-    float* line = reinterpret_cast<float*>(smem);  // [64]
-    float* T = line + kWave;                        // [B-1][K][G+4] when staged
+    double* line = reinterpret_cast<double*>(smem);   // [64] best path sums of one slot
+    float* T = reinterpret_cast<float*>(line + kWave);  // [B-1][K][G+4] when staged
     uint8_t* from = reinterpret_cast<uint8_t*>(
         T + (plan.stage ? (B - 1) * (int64_t)K * viterbi_stride<G>() : 0));
     const float* S0n = anchor_out ? xn + nS : nullptr;

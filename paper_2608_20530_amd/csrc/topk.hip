@@ -8,9 +8,10 @@
 //    issues its next tile's loads before it processes the current one.
 //  * Log-sum-exp: every element adds exp2(x*log2e - c) to a per-lane partial sum; c is a
 //    wave-uniform integer reference (log2 units), so moving it only rescales the partial sums by
-//    an exact power of two. c follows the top-K threshold value (a logit of the row, so the
-//    maximum's term stays at or above 2^-1) and is raised to the tile maximum in the rare case
-//    a tile sum exceeds 2^64.
+//    an exact power of two. c is set from the producer's first tile with a finite element (its
+//    maximum) and raised to a tile's maximum only when that tile's sum would exceed 2^64. Both
+//    depend on the producer's own data alone (not on when the threshold moves), so the sums, and
+//    the log-probabilities, are the same on every run.
 //  * Top-K: a wave-uniform threshold key T (published in LDS) screens every 16-byte chunk of a
 //    tile. bf16 chunks are screened with packed 16-bit integer max on the raw bit patterns (five
 //    instructions per 8 elements). The screen is strict (x > value of T) whenever every id in the
@@ -29,7 +30,12 @@
 //    wave-uniform and kept in scalar registers, so the per-tile control flow is scalar branches.
 //  * Rows split over several workgroups (small N*B) write partial results to the workspace and a
 //    second kernel merges them.
+//  * Every wait (a producer for ring space, the consumer for work) is bounded by a spin limit
+//    passed in at launch. A wait that gives up sets a bit in the status word at the start of the
+//    caller's workspace (the kernel still runs to its end, and that call's outputs are invalid);
+//    lilicorr_topk_wait_status reads and clears it.
 #include <hip/hip_runtime.h>
+#include <atomic>
 #include <climits>
 #include <type_traits>
 #include <math.h>
@@ -43,11 +49,20 @@ namespace {
 
 constexpr float kLog2eF = 1.44269504088896340736f;  // log2(e) rounded to fp32
 constexpr int kPerLane = 32;                         // elements per lane per tile
-constexpr int kRebase = 16;                          // max term exponent before the reference moves
 constexpr int kTopkWaves = 4;                        // wave 0 consumes, waves 1..3 produce
 constexpr int kProducers = kTopkWaves - 1;
 constexpr uint32_t kRing = 256;                      // staged chunks per producer ring (power of two)
-constexpr int kSpinLimit = 1 << 22;                  // bound on any wait (never reached)
+constexpr int kDefaultWaitLimit = 1 << 22;           // spins before a wait gives up (the default)
+constexpr size_t kStatusBytes = 256;                 // workspace header: the wait status word
+constexpr uint32_t kWaitTimedOut = 1u;               // status bit: a bounded wait gave up
+
+// Spin limit of the waits in kernels launched from now on (lilicorr_set_wait_limit).
+std::atomic<int> g_wait_limit{kDefaultWaitLimit};
+
+__device__ __forceinline__ void report_wait_timeout(uint32_t* status) {
+  if (lane_id() == 0)
+    __hip_atomic_fetch_or(status, kWaitTimedOut, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x2 __attribute__((ext_vector_type(2)));
@@ -216,18 +231,10 @@ struct Producer {
   int cref;         // (u) log2-units reference of the exp sums
   int cvalid;       // (u) cref is set
   float s;          // per-lane partial sum of exp2(x*log2e - cref)
-  uint64_t lastT;   // (u) threshold key the reference last followed
+  int limit;        // (u) spins before a wait for ring space gives up
+  uint32_t* status; // wait status word (workspace header)
 };
 
-__device__ __forceinline__ void rebase(Producer& pr, int need) {
-  if (!pr.cvalid) {
-    pr.cref = need;
-    pr.cvalid = 1;
-  } else if (need - pr.cref > kRebase) {
-    pr.s = ldexpf(pr.s, pr.cref - need);
-    pr.cref = need;
-  }
-}
 
 // Copy the chunks of the lanes with `live` set into this producer's ring (one 16-byte and one
 // 8-byte LDS store per lane), waiting for ring space if the consumer is behind.
@@ -238,11 +245,14 @@ __device__ __forceinline__ void stage_chunks(Producer& pr, TopkShared& sh, const
     // make everything written so far visible to the consumer before waiting for it
     if (lane_id() == 0)
       __hip_atomic_store(&sh.tail[pr.p], pr.tail, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    for (int spin = 0; spin < kSpinLimit; ++spin) {
+    for (int spin = 0; spin < pr.limit; ++spin) {
       pr.head = uniform32(__hip_atomic_load(&sh.head[pr.p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
       if (pr.tail + n - pr.head <= kRing) break;
       __builtin_amdgcn_s_sleep(1);
     }
+    // gave up: the chunks below overwrite slots the consumer has not read (memory-safe, as the
+    // ring index is masked); the call's outputs are invalid and the status word says so
+    if (pr.tail + n - pr.head > kRing) report_wait_timeout(pr.status);
   }
   if (live) {
     const uint32_t off = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -296,16 +306,11 @@ __device__ __forceinline__ uint64_t seed_from(Producer& pr, TopkShared& sh, uint
   return T;
 }
 
-// Exp sums of NE elements per lane. The reference follows the threshold value (an element's
-// value, so never above the row maximum); an element far above it shows up as a tile sum beyond
-// 2^kBig (or inf), and the tile is then summed again with the reference at the tile maximum.
+// Exp sums of NE elements per lane. The reference is the maximum of the producer's first tile
+// with a finite element; an element far above it shows up as a tile sum beyond kBig (or inf), and
+// the tile is then summed again with the reference at the tile maximum.
 template <int NE>
-__device__ __forceinline__ void exp_accumulate(Producer& pr, const float (&x)[NE], uint64_t T) {
-  // T is wave-uniform: the reference is computed on the vector unit and read back as a scalar
-  if (T != 0 && T != pr.lastT) {
-    rebase(pr, (int)uniform32((uint32_t)ref_for(key_value(T))));
-    pr.lastT = T;
-  }
+__device__ __forceinline__ void exp_accumulate(Producer& pr, const float (&x)[NE]) {
   float lane_max = -__builtin_inff();
   bool have_max = false;
   if (!pr.cvalid) {
@@ -313,7 +318,10 @@ __device__ __forceinline__ void exp_accumulate(Producer& pr, const float (&x)[NE
     for (int j = 0; j < NE; ++j) lane_max = fmaxf(lane_max, x[j]);
     have_max = true;
     const float m = wave_max_dpp(lane_max);
-    if (m > -__builtin_inff()) rebase(pr, (int)uniform32((uint32_t)ref_for(m)));
+    if (m > -__builtin_inff()) {
+      pr.cref = (int)uniform32((uint32_t)ref_for(m));
+      pr.cvalid = 1;
+    }
   }
   if (pr.cvalid) {
     float sum = tile_exp_sum(x, pr.cref);
@@ -409,7 +417,7 @@ __device__ __forceinline__ void produce_tile(Producer& pr, TopkShared& sh,
     }
     publish_tail(pr, sh);
   }
-  exp_accumulate<kPerLane>(pr, x, T);
+  exp_accumulate<kPerLane>(pr, x);
 }
 
 // ---- consumer ---------------------------------------------------------------------------------
@@ -479,8 +487,11 @@ __device__ __forceinline__ void consume_chunks(Consumer& c, TopkShared& sh, cons
   }
 }
 
+// Drains the rings until every producer is done and nothing is left; a run of `limit` empty polls
+// gives up and reports it in the status word.
 template <bool BF16>
-__device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K) {
+__device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K, int limit,
+                                            uint32_t* status) {
   const int lane = lane_id();
   // the consumer's batches are short and on the path of every producer's threshold: it takes
   // issue priority over the producer waves it shares a SIMD with
@@ -488,7 +499,8 @@ __device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K) 
   uint32_t head[kProducers];
 #pragma unroll
   for (int p = 0; p < kProducers; ++p) head[p] = 0;
-  for (int idle = 0; idle < kSpinLimit;) {
+  bool finished = false;
+  for (int idle = 0; idle < limit;) {
     bool any = false;
 #pragma unroll
     for (int p = 0; p < kProducers; ++p) {
@@ -520,12 +532,16 @@ __device__ __forceinline__ void consume_all(Consumer& c, TopkShared& sh, int K) 
 #pragma unroll
       for (int p = 0; p < kProducers; ++p)
         more |= uniform32(__hip_atomic_load(&sh.tail[p], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) != head[p];
-      if (!more) break;
+      if (!more) {
+        finished = true;
+        break;
+      }
       continue;
     }
     __builtin_amdgcn_s_sleep(2);
     ++idle;
   }
+  if (!finished) report_wait_timeout(status);
 }
 
 // Final outputs of a row from its merged sorted key list (one key per lane, lane 0 the best) and
@@ -554,7 +570,8 @@ __device__ __forceinline__ void write_row(uint64_t merged, double lse, int64_t r
 template <bool BF16>
 __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
     const void* __restrict__ logits, int64_t V, int K, int split, int32_t* __restrict__ ids,
-    float* __restrict__ logp, float* __restrict__ feat, unsigned char* __restrict__ partials) {
+    float* __restrict__ logp, float* __restrict__ feat, unsigned char* __restrict__ partials,
+    int wait_limit, uint32_t* __restrict__ status) {
   constexpr int EPC = ElemTraits<BF16>::kEPC;
   constexpr int U = kPerLane / EPC;
   constexpr int TILE = U * kWave;  // chunks per wave tile
@@ -600,7 +617,7 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
   cons.L = 0;
   cons.T_own = 0;
   if (wave == 0) {
-    consume_all<BF16>(cons, sh, K);
+    consume_all<BF16>(cons, sh, K, wait_limit, status);
   } else {
     Producer pr;
     pr.p = wave - 1;
@@ -610,7 +627,8 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
     pr.cref = 0;
     pr.cvalid = 0;
     pr.s = 0.f;
-    pr.lastT = 0;
+    pr.limit = wait_limit;
+    pr.status = status;
     // producer p streams tiles p, p + 3, p + 6, ... (the workgroup reads one contiguous window
     // at a time); its tiles come in increasing id order
     const uint32_t body_end_id = (uint32_t)(c_end * EPC - rowbase);
@@ -654,7 +672,7 @@ __global__ __launch_bounds__(kTopkWaves * kWave, 4) void topk_lse_kernel(
         stage_chunks(pr, sh, r, (uint32_t)(g - rowbase), 1u, live, m);
         publish_tail(pr, sh);
       }
-      exp_accumulate<1>(pr, x1, T);
+      exp_accumulate<1>(pr, x1);
     }
     const float ws = wave_sum(pr.s);
     if (lane == 0) {
@@ -1098,11 +1116,33 @@ bool topk_args_ok(int64_t N, int64_t B, int64_t V, int K) {
 
 using namespace lilicorr;
 
+// workspace: the status header, then (rows split over several workgroups) the partial results
+inline size_t topk_workspace_need(int64_t rows, int split, int K) {
+  return kStatusBytes + (split == 1 ? 0 : (size_t)rows * split * partial_stride(K));
+}
+
 extern "C" size_t lilicorr_topk_workspace_bytes(int64_t N, int64_t B, int64_t V, int K) {
   if (!topk_args_ok(N, B, V, K) || K > 64 || K > V) return 0;
-  int split = topk_split(N * B, V, true);
-  if (split == 1) return 0;
-  return (size_t)(N * B) * split * partial_stride(K);
+  return topk_workspace_need(N * B, topk_split(N * B, V, true), K);
+}
+
+extern "C" lilicorr_status lilicorr_topk_wait_status(const void* workspace, hipStream_t stream) {
+  if (!workspace) return LILICORR_ERR_INVALID_ARG;
+  if (!aligned16(workspace)) return LILICORR_ERR_ALIGNMENT;
+  uint32_t word = 0;
+  if (hipStreamSynchronize(stream) != hipSuccess) return LILICORR_ERR_HIP;
+  if (hipMemcpy(&word, workspace, sizeof word, hipMemcpyDeviceToHost) != hipSuccess)
+    return LILICORR_ERR_HIP;
+  if (word == 0) return LILICORR_OK;
+  const uint32_t zero = 0;
+  if (hipMemcpy(const_cast<void*>(workspace), &zero, sizeof zero, hipMemcpyHostToDevice) !=
+      hipSuccess)
+    return LILICORR_ERR_HIP;
+  return LILICORR_ERR_TIMEOUT;
+}
+
+extern "C" void lilicorr_set_wait_limit(int64_t spins) {
+  g_wait_limit.store(spins < 0 ? kDefaultWaitLimit : (int)(spins < INT_MAX ? spins : INT_MAX));
 }
 
 static lilicorr_status topk_launch(const void* logits, lilicorr_dtype dtype, int64_t N, int64_t B,
@@ -1117,13 +1157,15 @@ static lilicorr_status topk_launch(const void* logits, lilicorr_dtype dtype, int
   const bool bf16 = dtype == LILICORR_BF16;
   const int64_t rows = N * B;
   const int split = topk_split(rows, V, bf16);
-  const size_t need = split == 1 ? 0 : (size_t)rows * split * partial_stride(K);
-  if (need > 0 && (!workspace || workspace_bytes < need)) return LILICORR_ERR_WORKSPACE;
-  if (need > 0 && !aligned16(workspace)) return LILICORR_ERR_ALIGNMENT;
+  const size_t need = topk_workspace_need(rows, split, K);
+  if (!workspace || workspace_bytes < need) return LILICORR_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return LILICORR_ERR_ALIGNMENT;
   if (rows * split > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
 
   dim3 grid((unsigned)(rows * split)), block(kTopkWaves * kWave);
-  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  uint32_t* status = static_cast<uint32_t*>(workspace);
+  unsigned char* ws = static_cast<unsigned char*>(workspace) + kStatusBytes;
+  const int limit = g_wait_limit.load();
   const bool small = split > 1 && (V + split - 1) / split <= kSmallSpan;
   if (small && bf16)
     hipLaunchKernelGGL(topk_small_kernel<true>, grid, dim3(kSmallThreads), 0, stream, logits, V, K,
@@ -1133,10 +1175,10 @@ static lilicorr_status topk_launch(const void* logits, lilicorr_dtype dtype, int
                        K, split, ws);
   else if (bf16)
     hipLaunchKernelGGL(topk_lse_kernel<true>, grid, block, 0, stream, logits, V, K, split, ids, logp,
-                       feat, ws);
+                       feat, ws, limit, status);
   else
     hipLaunchKernelGGL(topk_lse_kernel<false>, grid, block, 0, stream, logits, V, K, split, ids,
-                       logp, feat, ws);
+                       logp, feat, ws, limit, status);
   if (launch_status() != LILICORR_OK) return LILICORR_ERR_HIP;
   if (split > 1) {
     hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)rows), dim3(kMergeThreads), 0, stream, ws, K, split,

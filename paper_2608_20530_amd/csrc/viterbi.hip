@@ -27,8 +27,8 @@ __global__ __launch_bounds__(kViterbiThreads) void viterbi_walk_kernel(
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint8_t* from = smem;                       // [B][K] predecessors
   uint8_t* path = from + B * K;               // [B]
-  float* line = reinterpret_cast<float*>(smem + ((B * K + B + 15) / 16) * 16);  // [64]
-  float* T = line + kWave;                    // [B-1][K][G+4] transposed scores when staged
+  double* line = reinterpret_cast<double*>(smem + ((B * K + B + 15) / 16) * 16);  // [64]
+  float* T = reinterpret_cast<float*>(line + kWave);  // [B-1][K][G+4] transposed scores (staged)
 
   const int64_t n = blockIdx.x;
   const int tid = threadIdx.x;
@@ -53,7 +53,7 @@ template <int G>
 void launch_viterbi(int64_t N, int64_t B, int K, hipStream_t stream, const float* S,
                     const float* S0, const float* logp, const int32_t* ids, float lambda,
                     int32_t* draft, int32_t* choice, float* logq, float* score) {
-  const size_t head = ((size_t)(B * K + B) + 15) / 16 * 16 + kWave * sizeof(float);
+  const size_t head = ((size_t)(B * K + B) + 15) / 16 * 16 + kWave * sizeof(double);
   const size_t t_bytes = (size_t)(B - 1) * K * viterbi_stride<G>() * sizeof(float);
   const bool stage = B > 1 && t_bytes <= kStageBytes;
   static const hipError_t attr = hipFuncSetAttribute(

@@ -4,10 +4,13 @@
 // g(c) = P_0[c_0] + sum_{t>=1} S[t-1][c_{t-1}][c_t] (+ lambda sum_t logp[t][c_t]), P_0 = S0 or all
 // zero. Wave 0 sweeps left to right with lane k holding the best score of a path ending at
 // candidate k: at each slot it scans the K predecessors in order (a strict '>' keeps the lowest
-// index on ties), in fp32 with one rounding per addition, and stores each lane's predecessor as a
-// byte. One lane picks the best final candidate (lowest index on ties) and traces back; then
-// groups of G lanes evaluate Eq. (localar) along the path for all slots in parallel. G >= K is
-// also the compile-time bound of the predecessor scan.
+// index on ties) and stores each lane's predecessor as a byte. Path sums are double: each fp32
+// score is widened exactly and every partial sum is rounded once, in the order of the sum above
+// (the lambda term, an exact product of two floats in double, after the slot's matching term), so
+// the maximiser is the exact one unless two path sums differ by less than that double rounding.
+// One lane picks the best final candidate (lowest index on ties) and traces back; then groups of
+// G lanes evaluate Eq. (localar) along the path for all slots in parallel. G >= K is also the
+// compile-time bound of the predecessor scan.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -17,11 +20,6 @@
 #include "common.hpp"
 
 namespace lilicorr {
-
-// v of `lane` (readlane reads the lane whatever the execution mask)
-__device__ __forceinline__ float lane_value(float v, int lane) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
-}
 
 // Row stride, in floats, of the transposed scores a workgroup stages for the sweep: column p of
 // S[t] for candidate k sits at T[(t*K + k) * stride + p], padded with -inf from K up to G; the
@@ -67,32 +65,34 @@ __device__ __forceinline__ void stage_transposed(float* T, const float* Sn, int6
 //   S0n    the request's anchor scores [K], or null for all zero
 //   lpn    its [B][K] drafter log-probabilities (read only when lambda != 0)
 //   idn    its [B][K] candidate ids
-//   from   B * K bytes of LDS, path B bytes of LDS, line 64 floats of LDS (16-byte aligned)
+//   from   B * K bytes of LDS, path B bytes of LDS, line 64 doubles of LDS (16-byte aligned)
 //   draft_n [B]; choice_n [B], logq_n [B], score_n [1] may be null
-// The sweep runs in wave 0 alone. Each slot's best scores are published through `line` (-inf for
-// lanes past K) and read back by every lane as 16-byte broadcasts; a wave's LDS operations
+// The sweep runs in wave 0 alone. Each slot's best path sums are published through `line` (-inf
+// for lanes past K) and read back by every lane as 16-byte broadcasts; a wave's LDS operations
 // complete in order, so no barrier is needed between that write and the reads. Candidates past K
 // score -inf against every predecessor, so the scan needs no test on K.
 template <int G, bool STAGED>
 __device__ __forceinline__ void viterbi_block(const float* Sv, const float* S0n, const float* lpn,
                                               const int32_t* idn, int64_t B, int K, float lambda,
-                                              uint8_t* from, uint8_t* path, float* line,
+                                              uint8_t* from, uint8_t* path, double* line,
                                               int32_t* draft_n, int32_t* choice_n, float* logq_n,
                                               float* score_n, int tid, int nthreads) {
   typedef float f4 __attribute__((ext_vector_type(4)));
+  typedef double d2 __attribute__((ext_vector_type(2)));
   constexpr int kStride = viterbi_stride<G>();
   const bool use_lp = lambda != 0.f;
+  const double lam = (double)lambda;
   if (tid < kWave) {
     const int k = tid;
     const bool live = k < K;
-    float best = -__builtin_inff();
+    double best = -__builtin_inf();
     if (live) {
-      best = S0n ? S0n[k] : 0.f;
-      if (use_lp) best = fmaf(lambda, lpn[k], best);
+      best = S0n ? (double)S0n[k] : 0.0;
+      if (use_lp) best += lam * (double)lpn[k];
     }
     for (int64_t t = 1; t < B; ++t) {
       line[k] = best;
-      float bv;
+      double bv;
       int bp = 0;
       if (STAGED) {
         // lane k's column of S[t-1] is row (t-1, k) of T; rows of dead lanes are not read
@@ -100,13 +100,14 @@ __device__ __forceinline__ void viterbi_block(const float* Sv, const float* S0n,
         f4 c4[G / 4];
 #pragma unroll
         for (int q = 0; q < G / 4; ++q) c4[q] = *reinterpret_cast<const f4*>(Tk + 4 * q);
-        bv = line[0] + c4[0][0];
+        bv = line[0] + (double)c4[0][0];
 #pragma unroll
         for (int q = 0; q < G / 4; ++q) {
-          const f4 b4 = *reinterpret_cast<const f4*>(line + 4 * q);
+          const d2 b01 = *reinterpret_cast<const d2*>(line + 4 * q);
+          const d2 b23 = *reinterpret_cast<const d2*>(line + 4 * q + 2);
 #pragma unroll
           for (int e = (q == 0 ? 1 : 0); e < 4; ++e) {
-            const float v = b4[e] + c4[q][e];
+            const double v = (e < 2 ? b01[e & 1] : b23[e & 1]) + (double)c4[q][e];
             if (v > bv) {
               bv = v;
               bp = 4 * q + e;
@@ -115,9 +116,9 @@ __device__ __forceinline__ void viterbi_block(const float* Sv, const float* S0n,
         }
       } else {
         const float* St = Sv + (t - 1) * (int64_t)K * K;
-        bv = line[0] + (live ? St[k] : 0.f);
+        bv = line[0] + (double)(live ? St[k] : 0.f);
         for (int p = 1; p < K; ++p) {
-          const float v = line[p] + (live ? St[p * K + k] : 0.f);
+          const double v = line[p] + (double)(live ? St[p * K + k] : 0.f);
           if (v > bv) {
             bv = v;
             bp = p;
@@ -125,30 +126,30 @@ __device__ __forceinline__ void viterbi_block(const float* Sv, const float* S0n,
         }
       }
       if (live) {
-        if (use_lp) bv = fmaf(lambda, lpn[t * K + k], bv);
+        if (use_lp) bv += lam * (double)lpn[t * K + k];
         from[t * K + k] = (uint8_t)bp;
       } else {
-        bv = -__builtin_inff();
+        bv = -__builtin_inf();
       }
       best = bv;
     }
     // best final candidate (lowest index on ties), the same scan in every lane
     line[k] = best;
     int c = 0;
-    float g = line[0];
+    double g = line[0];
 #pragma unroll
-    for (int q = 0; q < G / 4; ++q) {
-      const f4 b4 = *reinterpret_cast<const f4*>(line + 4 * q);
+    for (int q = 0; q < G / 2; ++q) {
+      const d2 b2 = *reinterpret_cast<const d2*>(line + 2 * q);
 #pragma unroll
-      for (int e = (q == 0 ? 1 : 0); e < 4; ++e) {
-        if (b4[e] > g) {
-          g = b4[e];
-          c = 4 * q + e;
+      for (int e = (q == 0 ? 1 : 0); e < 2; ++e) {
+        if (b2[e] > g) {
+          g = b2[e];
+          c = 2 * q + e;
         }
       }
     }
     if (k == 0) {
-      if (score_n) *score_n = g;
+      if (score_n) *score_n = (float)g;
       path[B - 1] = (uint8_t)c;
       for (int64_t t = B - 1; t >= 1; --t) {
         c = from[t * K + c];

@@ -46,3 +46,26 @@ def cfg_inputs():
         return _CFG_CACHE[i]
 
     return get
+
+
+_CHAIN_CACHE = {}
+
+
+@pytest.fixture(scope="session")
+def oracle_chain(cfg_inputs):
+    """oracle_chain(i) -> the oracle chain of every request of workload i (parity.oracle_chain_all),
+    computed once per session on a thread pool."""
+    import time
+
+    from parity import oracle_chain_all, oracle_threads
+
+    def get(i):
+        if i not in _CHAIN_CACHE:
+            cfg, inp = cfg_inputs(i)
+            t0 = time.perf_counter()
+            _CHAIN_CACHE[i] = oracle_chain_all(cfg, inp)
+            print(f"oracle chain of config {i} ({cfg.N} requests) in "
+                  f"{time.perf_counter() - t0:.1f} s on {oracle_threads()} threads", flush=True)
+        return _CHAIN_CACHE[i]
+
+    return get

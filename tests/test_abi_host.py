@@ -31,7 +31,8 @@ def test_header_declares_the_path(L):
               "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes", "lilicorr_score_walk_workspace_bytes",
               "lilicorr_score_walk_certified", "lilicorr_score_walk_certified_workspace_bytes",
               "lilicorr_block_graph_create", "lilicorr_block_graph_launch",
-              "lilicorr_block_graph_destroy", "lilicorr_status_string"]:
+              "lilicorr_block_graph_destroy", "lilicorr_status_string",
+              "lilicorr_topk_wait_status", "lilicorr_set_wait_limit"]:
         assert n in names
 
 
@@ -43,7 +44,7 @@ def test_every_declared_symbol_is_exported(L):
 
 def test_status_strings(L):
     assert L.lilicorr_status_string(0) == "ok"
-    for code in (-1, -2, -3, -4, -5):
+    for code in (-1, -2, -3, -4, -5, -6):
         assert L.lilicorr_status_string(code) not in ("ok", "unknown status")
     assert L.lilicorr_status_string(-99) == "unknown status"
 
@@ -56,23 +57,25 @@ def test_size_queries(L):
     assert L.lilicorr_packed_weight_bytes(80) == 2 * 3 * 128 * 128 * 2 + 2 * 80 * 80 * 4
     assert L.lilicorr_packed_weight_bytes(8) == 0
     assert L.lilicorr_packed_weight_bytes(2048) == 0
-    # headline shapes run one workgroup per row: no workspace
-    assert L.lilicorr_topk_workspace_bytes(64, 16, 151936, 16) == 0
-    assert L.lilicorr_topk_workspace_bytes(256, 16, 262144, 32) == 0
+    # headline shapes run one workgroup per row: the workspace is the 256-byte status header
+    H = 256
+    assert L.lilicorr_topk_workspace_bytes(64, 16, 151936, 16) == H
+    assert L.lilicorr_topk_workspace_bytes(256, 16, 262144, 32) == H
     # a single request is split over several workgroups per row
-    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) > 0
+    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) > H
     assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 65) == 0
-    # the split rule, through the workspace size (rows x segments x (16-byte header + K keys)):
-    # few rows whose short segments (<= 8192 logits) all run at once take ceil(V / 8192) of them
+    # the split rule, through the workspace size (header, then rows x segments x (16-byte
+    # partial header + K keys)): few rows whose short segments (<= 8192 logits) all run at once
+    # take ceil(V / 8192) of them
     part = lambda K: 16 + 8 * K
-    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) == 16 * 19 * part(8)
-    assert L.lilicorr_topk_workspace_bytes(1, 8, 32000, 4) == 8 * 4 * part(4)
-    assert L.lilicorr_topk_workspace_bytes(1, 1, 300000, 64) == 37 * part(64)
+    assert L.lilicorr_topk_workspace_bytes(1, 16, 151936, 8) == H + 16 * 19 * part(8)
+    assert L.lilicorr_topk_workspace_bytes(1, 8, 32000, 4) == H + 8 * 4 * part(4)
+    assert L.lilicorr_topk_workspace_bytes(1, 1, 300000, 64) == H + 37 * part(64)
     # more rows x segments than run at once: streaming segments of >= 12288 logits
-    assert L.lilicorr_topk_workspace_bytes(2, 16, 151936, 16) == 32 * 12 * part(16)
-    assert L.lilicorr_topk_workspace_bytes(16, 16, 151936, 16) == 256 * 4 * part(16)
+    assert L.lilicorr_topk_workspace_bytes(2, 16, 151936, 16) == H + 32 * 12 * part(16)
+    assert L.lilicorr_topk_workspace_bytes(16, 16, 151936, 16) == H + 256 * 4 * part(16)
     # rows shorter than one short segment stay whole
-    assert L.lilicorr_topk_workspace_bytes(1, 2, 5000, 8) == 0
+    assert L.lilicorr_topk_workspace_bytes(1, 2, 5000, 8) == H
 
 
 A = 4096  # a fake, 16-byte aligned "device" address: never dereferenced on these paths
@@ -80,7 +83,7 @@ A = 4096  # a fake, 16-byte aligned "device" address: never dereferenced on thes
 
 def test_topk_argument_errors(L):
     lib = L.load_library()
-    ok = (A, 1, 2, 3, 1000, 8, A, A, None, 0, None)
+    ok = (A, 1, 2, 3, 1000, 8, A, A, A, 256, None)
     def call(i, v):
         args = list(ok)
         args[i] = v
@@ -96,10 +99,20 @@ def test_topk_argument_errors(L):
     assert call(5, 65) == -2            # K > 64
     assert call(5, 1001) == -2          # K > V
     assert call(0, A + 2) == -3         # alignment
-    # N*B*V that would need workspace, none given
+    # every call needs the workspace's status header; split rows need room for partials too
+    assert call(9, 255) == -4           # workspace_bytes below the 256-byte header
+    assert call(8, A + 4) == -3         # workspace alignment (with enough bytes)
     args = list(ok)
     args[2], args[3], args[4] = 1, 1, 151936
     assert lib.lilicorr_topk(*args) == -4
+    args[9] = 256
+    assert lib.lilicorr_topk(*args) == -4
+
+
+def test_wait_status_argument_errors(L):
+    lib = L.load_library()
+    assert lib.lilicorr_topk_wait_status(None, None) == -1
+    assert lib.lilicorr_topk_wait_status(A + 4, None) == -3
 
 
 def test_topk_features_argument_errors(L):
