@@ -220,6 +220,27 @@ lilicorr_status lilicorr_score_walk(const int32_t *ids, const float *logp, const
                                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * lilicorr_score_walk without a workspace, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid allocation). Same
+ * arguments, results, limits and errors as lilicorr_score_walk, minus the workspace: its
+ * counters and walk table live in an 8 MiB array the library holds on each GPU it runs on, from
+ * the first call on that GPU until the process ends. The call allocates nothing (no hipMalloc,
+ * no library allocation); it zeroes its counters with a small kernel on `stream` before the pass
+ * (no memset node, so it can be recorded into a graph). All calls on one GPU share that array:
+ * calls that overlap in time on one GPU (another stream, another thread) race and give wrong
+ * results. LILICORR_ERR_WORKSPACE when the call would need more than the array holds, i.e. when
+ * lilicorr_score_walk_workspace_bytes(N, B, K) > 8 MiB (about 4,300 requests of 16 slots x 16
+ * candidates); LILICORR_ERR_HIP if the array's device address cannot be obtained.
+ */
+lilicorr_status lilicorr_score_walk_noalloc(const int32_t *ids, const float *logp, const void *E,
+                                            lilicorr_dtype e_dtype, int64_t V, int d,
+                                            const void *packed_w, const float *anchor_out,
+                                            int64_t N, int64_t B, int K, float sigma,
+                                            float logp_weight, float *S, float *S0,
+                                            int32_t *draft, int32_t *choice, float *logq,
+                                            hipStream_t stream);
+
+/*
  * lilicorr_score_walk with certified decisions. The greedy rule (Sec. 3.5) commits the candidate
  * with the largest matching score of Eq. (pair); the pass computes those scores in fp32, whose
  * error can reorder two nearly equal scores. Here every walk decision whose fp32 winner is

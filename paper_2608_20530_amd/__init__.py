@@ -11,6 +11,7 @@ The four steps run in hand-written HIP kernels behind a C ABI (include/lilicorr.
   lilicorr_greedy_walk        S, S0, logp, ids -> draft, choice, logq   (Sec. 3.5, Eq. localar)
   lilicorr_viterbi_walk       S, S0, logp, ids -> best path, logq, g    (Eq. pathscore)
   lilicorr_score_walk         ids, logp, E -> draft, choice, logq       (steps 2-4 in one pass)
+  lilicorr_score_walk_noalloc the same pass with no workspace (library-held device scratch)
   lilicorr_score_walk_certified  the same pass, near-tied decisions decided again in fp64
   lilicorr_score_viterbi      the same pass with the exact max-path decode
   lilicorr_block_graph_*      top-K + one fused pass recorded as one HIP graph, replayed per block
@@ -33,6 +34,7 @@ __all__ = [
     "lilicorr_topk_wait_status", "lilicorr_set_wait_limit", "lilicorr_packed_weight_bytes",
     "lilicorr_pack_weights", "lilicorr_candidate_vectors", "lilicorr_pair_scores",
     "lilicorr_greedy_walk", "lilicorr_viterbi_walk", "lilicorr_score_walk", "lilicorr_score_walk_workspace_bytes",
+    "lilicorr_score_walk_noalloc",
     "lilicorr_score_walk_certified", "lilicorr_score_walk_certified_workspace_bytes",
     "lilicorr_score_viterbi", "lilicorr_score_viterbi_workspace_bytes",
     "lilicorr_block_graph_create", "lilicorr_block_graph_launch", "lilicorr_block_graph_destroy",
@@ -109,6 +111,8 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_score_walk_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_walk": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, SZ,
                                  P], I),
+        "lilicorr_score_walk_noalloc": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P,
+                                         P], I),
         "lilicorr_score_walk_certified_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_walk_certified": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, F, P, P, P,
                                            P, P, P, P, SZ, P], I),
@@ -211,6 +215,12 @@ def lilicorr_score_walk(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
     return _call("lilicorr_score_walk", ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
                  K, sigma, logp_weight, S, S0, draft, choice, logq, workspace, workspace_bytes,
                  stream)
+
+
+def lilicorr_score_walk_noalloc(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K,
+                                sigma, logp_weight, S, S0, draft, choice, logq, stream):
+    return _call("lilicorr_score_walk_noalloc", ids, logp, E, e_dtype, V, d, packed_w, anchor_out,
+                 N, B, K, sigma, logp_weight, S, S0, draft, choice, logq, stream)
 
 
 def lilicorr_score_walk_certified_workspace_bytes(N: int, B: int, K: int) -> int:

@@ -26,6 +26,8 @@
 // of another candidate and records the contenders; in step 6 the last workgroup decides each
 // flagged row it meets on the path again in double precision (certify.hpp).
 #include <hip/hip_runtime.h>
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 #include <math.h>
 #include <stdint.h>
@@ -488,7 +490,7 @@ inline bool fused_shape_ok(int64_t N, int64_t B, int K, bool exact) {
   return B <= kMaxTableRows && 1 + (B - 1) * (int64_t)K <= kMaxTableRows;
 }
 
-template <bool EXACT, bool CERT>
+template <bool EXACT, bool CERT, bool CHECK_ONLY = false>
 lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const void* E,
                                  lilicorr_dtype e_dtype, int64_t V, int d, const void* packed_w,
                                  const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
@@ -521,6 +523,7 @@ lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const vo
   if (anchor_out) plan.wg += 1;
   if (N > 0x7fffffffll / plan.wg) return LILICORR_ERR_UNSUPPORTED;
   if (plan.lds_bytes > 160 * 1024) return LILICORR_ERR_UNSUPPORTED;
+  if (CHECK_ONLY) return LILICORR_OK;
   const VecGeom g = vec_geom(d);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
@@ -547,10 +550,82 @@ lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const vo
   return launch_status();
 }
 
+// ---- allocation-free variant of the greedy pass -------------------------------------------------
+// Its counters and table live in `scratch`, a file-scope device array (one copy per GPU, held
+// until the process ends). Host code never passes the array's name to a kernel: at the first call
+// on a device, with that device current, the array's device address is looked up once and kept
+// per device; every later use goes through that address.
+constexpr size_t kNoAllocScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<unsigned char*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The device address of `scratch` on the current device, looked up once per device; null (and
+// *err set) if the lookup fails.
+unsigned char* scratch_address(lilicorr_status* err) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    *err = LILICORR_ERR_HIP;
+    return nullptr;
+  }
+  unsigned char* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p) return p;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+  if (!p) {
+    void* addr = nullptr;
+    if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) {
+      *err = LILICORR_ERR_HIP;
+      return nullptr;
+    }
+    p = static_cast<unsigned char*>(addr);
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  return p;
+}
+
+// Zeroes n 32-bit words (the ticket counters) before the pass: a kernel rather than a memset, so
+// the call can be recorded into a graph.
+__global__ __launch_bounds__(256) void clear_words_kernel(uint32_t* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    p[i] = 0u;
+}
+
 }  // namespace
 }  // namespace lilicorr
 
 using namespace lilicorr;
+
+extern "C" lilicorr_status lilicorr_score_walk_noalloc(
+    const int32_t* ids, const float* logp, const void* E, lilicorr_dtype e_dtype, int64_t V, int d,
+    const void* packed_w, const float* anchor_out, int64_t N, int64_t B, int K, float sigma,
+    float logp_weight, float* S, float* S0, int32_t* draft, int32_t* choice, float* logq,
+    hipStream_t stream) {
+  // the limits and argument checks of lilicorr_score_walk come first (its own status codes);
+  // then the scratch size
+  if (!ids || !logp || !E || !packed_w || !draft) return LILICORR_ERR_INVALID_ARG;
+  if (!fused_shape_ok(N, B, K, false)) return N < 1 || B < 1 || K < 1 ? LILICORR_ERR_INVALID_ARG
+                                                                        : LILICORR_ERR_UNSUPPORTED;
+  const size_t need = fused_workspace_bytes(N, B, K, false);
+  if (need > kNoAllocScratchBytes) return LILICORR_ERR_WORKSPACE;
+  lilicorr_status err = LILICORR_OK;
+  unsigned char* ws = scratch_address(&err);
+  if (!ws) return err;
+  // validate everything before launching the clear (a rejected call launches nothing)
+  const lilicorr_status pre = score_and_decode<false, false, true>(
+      ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B, K, sigma, logp_weight, 0.f, S, S0,
+      draft, choice, logq, nullptr, nullptr, ws, need, stream);
+  if (pre != LILICORR_OK) return pre;
+  const int64_t words = (int64_t)(counter_bytes(N) / 4);
+  hipLaunchKernelGGL(clear_words_kernel, dim3((unsigned)((words + 255) / 256 < 64 ? (words + 255) / 256 : 64)),
+                     dim3(256), 0, stream, reinterpret_cast<uint32_t*>(ws), words);
+  if (launch_status() != LILICORR_OK) return LILICORR_ERR_HIP;
+  return score_and_decode<false, false>(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N, B,
+                                        K, sigma, logp_weight, 0.f, S, S0, draft, choice, logq,
+                                        nullptr, nullptr, ws, need, stream);
+}
 
 extern "C" size_t lilicorr_score_walk_workspace_bytes(int64_t N, int64_t B, int K) {
   return fused_shape_ok(N, B, K, false) ? fused_workspace_bytes(N, B, K, false) : 0;
