@@ -55,6 +55,9 @@ def parse():
                     help="skip the per-workload line (both metrics at every workload)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
+    ap.add_argument("--logits-only", choices=["headline", "stress"],
+                    help="only the logits pass at one workload (for profiling runs): prints its "
+                         "line and exits")
     return ap.parse_args()
 
 
@@ -351,6 +354,24 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     L.load_library()
+
+    if args.logits_only:
+        c = workloads.config(3 if args.logits_only == "headline" else 4)
+        lg = workloads.make_logits(c).cuda()
+        bufs = [lg] + [lg.clone() for _ in range(ROTATE - 1)] if c.index == 3 else [lg]
+        t, lo, hi = time_logits_pass(L, torch, c, bufs, iters=100 if c.index == 3 else 20)
+        nb = c.N * c.B * c.V * 2 + c.N * c.B * c.K * 8
+        if args.calibrate_copy:
+            src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+            dst = torch.empty_like(src)
+            for _ in range(3):
+                dst.copy_(src)
+            torch.cuda.synchronize()
+        print(json.dumps({"logits_pass": c.name, "us": t * 1e6, "us_batch_min": lo * 1e6,
+                          "us_batch_max": hi * 1e6, "GB_s": nb / t / 1e9,
+                          "frac_of_8TBs": nb / t / 1e9 / PEAK_HBM_GBS,
+                          "algorithmic_bytes_per_launch": nb}), flush=True)
+        return
 
     cfg = workloads.config(3)
     t_gen = time.perf_counter()
