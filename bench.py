@@ -55,6 +55,10 @@ def parse():
                     help="skip the per-workload line (both metrics at every workload)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
+    ap.add_argument("--workload-step", choices=["tiny", "single", "tiers16", "headline64",
+                                                "stress256"],
+                    help="only the per-workload step at one workload (for profiling runs): "
+                         "prints its line and exits")
     ap.add_argument("--logits-only", choices=["headline", "stress"],
                     help="only the logits pass at one workload (for profiling runs): prints its "
                          "line and exits")
@@ -78,7 +82,7 @@ def traffic_per_launch():
 
 
 def time_logits_pass(L, torch, cfg, logits_list, iters, batches=5):
-    """Logits-pass duration (s) at one workload: after one untimed batch, `batches` batches of
+    """Logits-pass duration (s) at one workload: after three untimed batches, `batches` batches of
     `iters` back-to-back launches over the rotating buffers, each between two HIP events on the
     launch stream; returns the mean, smallest and largest per-launch mean of the batches."""
     K = cfg.K
@@ -102,7 +106,8 @@ def time_logits_pass(L, torch, cfg, logits_list, iters, batches=5):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / 1e3 / iters
 
-    batch()
+    for _ in range(3):
+        batch()
     t = [batch() for _ in range(batches)]
     if L.topk_wait_status(ws) != 0:
         raise RuntimeError("a bounded wait of the logits pass gave up: outputs invalid")
@@ -168,9 +173,10 @@ def median_launch_us(torch, fn, iters=50, warmup=5):
 
 def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
     """Both metrics at one workload: blocks/s of the step (logits pass, then the fused pass or the
-    separate calls) and the logits pass's GB/s, each the mean over `iters` back-to-back calls
-    between two HIP events. The logits rotate over enough resident copies (at least 1 GiB in all)
-    that every call reads its logits from HBM, as in the headline loop."""
+    separate calls, through the C ABI with arguments marshalled once) and the logits pass's GB/s,
+    each the mean over `iters` back-to-back calls between two HIP events. The logits rotate over
+    enough resident copies (at least 1 GiB in all) that every call reads its logits from HBM, as in
+    the headline loop."""
     lg = inp["logits"].cuda()
     nbytes = lg.numel() * lg.element_size()
     copies = max(1, min(1024, -(-(1 << 30) // nbytes)))
@@ -185,25 +191,46 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
     choice = torch.empty_like(draft)
     logq = torch.empty(N, B, dtype=torch.float32, device="cuda")
     # the fused pass holds both sides' fp32 projections in LDS (bf16 tables, d <= 256); other
-    # workloads take the separate calls
+    # workloads take the separate calls. Every call goes straight to the C ABI with its arguments
+    # marshalled once, as in the headline loop.
+    lib = L.load_library()
+    st = torch.cuda.current_stream().cuda_stream
+    e_code = L.BF16 if E.dtype == torch.bfloat16 else L.F32
+    l_code = L.BF16 if lg.dtype == torch.bfloat16 else L.F32
     fused = E.dtype == torch.bfloat16 and c.d <= 256
     if fused:
         ws_fused = L.score_walk_workspace(N, B, K)
+        walk_args = (ids.data_ptr(), logp.data_ptr(), E.data_ptr(), e_code, V, c.d,
+                     packed.data_ptr(), None, N, B, K, L.SIGMA, 0.0, None, None, draft.data_ptr(),
+                     choice.data_ptr(), logq.data_ptr(), ws_fused.data_ptr(), ws_fused.numel(), st)
 
         def rest():
-            L.score_walk(ids, logp, E, packed, None, L.SIGMA, 0.0, out=(draft, choice, logq),
-                         workspace=ws_fused)
+            if lib.lilicorr_score_walk(*walk_args) != 0:
+                raise RuntimeError("lilicorr_score_walk failed")
     else:
         in_vec = torch.empty(N, B, K, c.d, dtype=torch.float32, device="cuda")
         out_vec = torch.empty_like(in_vec)
         S = torch.empty(N, max(B - 1, 1), K, K, dtype=torch.float32, device="cuda")
+        cv_args = (ids.data_ptr(), E.data_ptr(), e_code, V, c.d, packed.data_ptr(), N, B, K,
+                   in_vec.data_ptr(), out_vec.data_ptr(), st)
+        ps_args = (in_vec.data_ptr(), out_vec.data_ptr(), None, N, B, K, c.d, L.SIGMA,
+                   S.data_ptr() if B > 1 else None, None, st)
+        gw_args = (S.data_ptr() if B > 1 else None, None, logp.data_ptr(), ids.data_ptr(), N, B,
+                   K, 0.0, draft.data_ptr(), choice.data_ptr(), logq.data_ptr(), st)
 
         def rest():
-            L.candidate_vectors(ids, E, packed, out=(in_vec, out_vec))
-            L.pair_scores(in_vec, out_vec, None, L.SIGMA, out=(S, None))
-            L.greedy_walk(S, None, logp, ids, 0.0, out=(draft, choice, logq))
+            if (lib.lilicorr_candidate_vectors(*cv_args) != 0 or
+                    lib.lilicorr_pair_scores(*ps_args) != 0 or
+                    lib.lilicorr_greedy_walk(*gw_args) != 0):
+                raise RuntimeError("separate calls failed")
 
-    topk = lambda i: L.topk(lgs[i % copies], K, out=(ids, logp), workspace=ws)
+    tk_args = [(x.data_ptr(), l_code, N, B, V, K, ids.data_ptr(), logp.data_ptr(), ws.data_ptr(),
+                ws.numel(), st) for x in lgs]
+
+    def topk(i):
+        if lib.lilicorr_topk(*tk_args[i % copies]) != 0:
+            raise RuntimeError("lilicorr_topk failed")
+
     counter = [0]
 
     def batch(fn):
@@ -223,6 +250,8 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
         counter[0] += 1
     step = batch(lambda i: (topk(i), rest()))
     t_topk = batch(topk)
+    if L.topk_wait_status(ws) != 0:
+        raise RuntimeError("a bounded wait of the logits pass gave up: outputs invalid")
     return {"workload": f"{c.name}: N={N}, B={B}, K={K}, V={V}, d={c.d}, "
                         f"{'bf16' if lg.element_size() == 2 else 'fp32'} logits",
             "path": "lilicorr_topk -> " + ("lilicorr_score_walk" if fused else
@@ -355,6 +384,13 @@ def main():
         sys.exit(1)
     L.load_library()
 
+    if args.workload_step:
+        c = next(c for c in workloads.CONFIGS if c.name == args.workload_step)
+        print(json.dumps({"per_workload": {c.name: per_config_rates(L, torch, c,
+                                                                    workloads.make_inputs(c))}}),
+              flush=True)
+        return
+
     if args.logits_only:
         c = workloads.config(3 if args.logits_only == "headline" else 4)
         lg = workloads.make_logits(c).cuda()
@@ -449,11 +485,12 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / 1e3 / reps
 
-    # Bring the GPU to its working clock (the inputs were just generated on the host and the
-    # GPU sat idle): 200 logits passes, untimed. Then the logits pass alone, timed, for the
-    # roofline entry; then each way through the block: W untimed steps, K timed steps.
+    # Bring the GPU to its working clock (the inputs were just generated on the host and the GPU
+    # sat idle; the first few hundred passes run through a clock dip): 1000 logits passes (~50
+    # ms), untimed. Then the logits pass alone, timed, for the roofline entry; then each way
+    # through the block: W untimed steps, K timed steps.
     reps = 200
-    topk_batch(reps)
+    topk_batch(1000)
     topk_s = topk_batch(reps)
     for i in range(args.warmup):
         step(i)
@@ -566,7 +603,7 @@ def main():
         out["logits_pass"] = {
             "method": "per-launch mean over batches of back-to-back launches (100 at the "
                       "headline over 4 rotating buffers, 20 at the stress shape), 5 batches "
-                      "after one untimed batch; HIP events on the launch stream",
+                      "after three untimed batches; HIP events on the launch stream",
             "headline": {"GB_s": algo_bytes / t3 / 1e9, "us": t3 * 1e6,
                          "us_batch_min": lo3 * 1e6, "us_batch_max": hi3 * 1e6,
                          "frac_of_8TBs": algo_bytes / t3 / 1e9 / PEAK_HBM_GBS,

@@ -174,8 +174,8 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   const size_t slice = (size_t)nbp * 1024;
   const unsigned char* wf = frags + (size_t)(lside == 0 ? 1 : 0) * dkp * 3 * slice +
                             (size_t)cg * kNbPerWave * 1024 + lane * 16;
-  BFrag b0;
-  if (side_rows > 0) load_bfrag(b0, wf, slice, 0);  // in flight during the gather
+  BFrag<kNbPerWave> b0;
+  if (side_rows > 0) load_bfrag<kNbPerWave>(b0, wf, slice, 0);  // in flight during the gather
   // tile row r holds candidate r % K of slot s0 + r / K; the out side reads tile rows
   // [0, 64), the in side tile rows [K, K + 64). Rows outside the workgroup's slots are zero (the
   // anchor workgroup has only in rows, of slot 0: s0 = -1).
@@ -198,9 +198,9 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   // ---- 2. projection --------------------------------------------------------------------------
   f32x4 acc[kSideRm][kNbPerWave];
   if (side_rows > 0) {
-    project_tile<kSideRm>(acc, b0, A + lside * K * plan.astride, plan.astride, wf, slice, dkp,
-                          lane);
-    row_sumsq<kSideRm>(acc, ssw + (lside * plan.ws + cg) * kSideRows, lane);
+    project_tile<kSideRm, kNbPerWave>(acc, b0, A + lside * K * plan.astride, plan.astride, wf,
+                                      slice, dkp, lane);
+    row_sumsq<kSideRm, kNbPerWave>(acc, ssw + (lside * plan.ws + cg) * kSideRows, lane);
   }
   __syncthreads();  // every wave is done reading the gathered tile
 

@@ -24,7 +24,10 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kNbPerWave = 4;  // 16-column blocks owned by each wave
+// The packed layout pads the output columns to whole groups of kNbPerWave 16-column blocks (the
+// candidate-vector kernel's waves own one group each); a kernel may give its waves fewer blocks
+// (NB, a divisor of kNbPerWave) and so run more waves over the same layout.
+constexpr int kNbPerWave = 4;
 
 struct VecGeom {
   int d16;    // 16-column blocks of the output
@@ -58,24 +61,26 @@ inline size_t frag_bytes(int d) {
 
 inline size_t packed_bytes(int d) { return frag_bytes(d) + (size_t)2 * d * d * sizeof(float); }
 
-typedef u32x4 BFrag[kNbPerWave][3];
+template <int NB = kNbPerWave>
+using BFrag = u32x4[NB][3];
 
-// B fragments of k-block kb for a wave's four column blocks, three terms each; wf points at the
+// B fragments of k-block kb for a wave's NB column blocks, three terms each; wf points at the
 // wave's first column block (plus lane * 16) in k-block 0, term 0 of its side
-__device__ __forceinline__ void load_bfrag(BFrag& dst, const unsigned char* wf, size_t slice,
+template <int NB>
+__device__ __forceinline__ void load_bfrag(BFrag<NB>& dst, const unsigned char* wf, size_t slice,
                                            int kb) {
   const unsigned char* p = wf + (size_t)kb * 3 * slice;
 #pragma unroll
   for (int t = 0; t < 3; ++t)
 #pragma unroll
-    for (int nb = 0; nb < kNbPerWave; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
       dst[nb][t] = *reinterpret_cast<const u32x4*>(p + t * slice + nb * 1024);
 }
 
 // acc[mb][nb] += A[rows of block mb][k-block kb] x B[k-block kb][column block nb], all three
 // terms; the term loop is outermost so consecutive MFMAs never feed each other
-template <int RM>
-__device__ __forceinline__ void mfma_kblock(f32x4 (&acc)[RM][kNbPerWave], const BFrag& b,
+template <int RM, int NB>
+__device__ __forceinline__ void mfma_kblock(f32x4 (&acc)[RM][NB], const BFrag<NB>& b,
                                             const uint16_t* A, int astride, int kb, int lane) {
   bf16x8 a[RM];
   const int kcol = kb * 32 + (lane >> 4) * 8;
@@ -88,36 +93,36 @@ __device__ __forceinline__ void mfma_kblock(f32x4 (&acc)[RM][kNbPerWave], const 
 #pragma unroll
     for (int mb = 0; mb < RM; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb)
+      for (int nb = 0; nb < NB; ++nb)
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             a[mb], __builtin_bit_cast(bf16x8, b[nb][t]), acc[mb][nb], 0, 0, 0);
 }
 
-// The whole contraction of a wave's RM row blocks x four column blocks. b0 must already hold
+// The whole contraction of a wave's RM row blocks x NB column blocks. b0 must already hold
 // k-block 0 (so its loads can overlap whatever precedes). Two k-blocks per trip through two
 // register buffers: the loads of the next k-block are in flight while the MFMAs of the current
 // one run (the last trip reloads the final k-block instead of reading past the weights).
-template <int RM>
-__device__ __forceinline__ void project_tile(f32x4 (&acc)[RM][kNbPerWave], BFrag& b0,
+template <int RM, int NB>
+__device__ __forceinline__ void project_tile(f32x4 (&acc)[RM][NB], BFrag<NB>& b0,
                                              const uint16_t* A, int astride,
                                              const unsigned char* wf, size_t slice, int dkp,
                                              int lane) {
 #pragma unroll
   for (int mb = 0; mb < RM; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  BFrag b1;
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  BFrag<NB> b1;
   // the scheduling barriers keep each k-block's twelve fragment loads issued together ahead of
   // the MFMAs of the previous one: left alone, the scheduler interleaves them into the MFMA
   // stream to save registers and then waits on loads it has just issued
   for (int kb = 0; kb < dkp; kb += 2) {
     load_bfrag(b1, wf, slice, kb + 1);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_kblock<RM>(acc, b0, A, astride, kb, lane);
+    mfma_kblock<RM, NB>(acc, b0, A, astride, kb, lane);
     __builtin_amdgcn_sched_barrier(0);
     load_bfrag(b0, wf, slice, kb + 2 < dkp ? kb + 2 : dkp - 1);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_kblock<RM>(acc, b1, A, astride, kb + 1, lane);
+    mfma_kblock<RM, NB>(acc, b1, A, astride, kb + 1, lane);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -154,17 +159,16 @@ __device__ __forceinline__ void gather_rows(uint16_t* A, int astride, int rows,
 
 // Per-wave partial squared norms of the tile's rows: lane l holds rows (l/16)*4 + i of each row
 // block and column l%16 of each column block (padding columns hold zeros); ss[row] receives the
-// sum over this wave's 64 columns.
-template <int RM>
-__device__ __forceinline__ void row_sumsq(const f32x4 (&acc)[RM][kNbPerWave], float* ss,
-                                          int lane) {
+// sum over this wave's NB * 16 columns.
+template <int RM, int NB>
+__device__ __forceinline__ void row_sumsq(const f32x4 (&acc)[RM][NB], float* ss, int lane) {
 #pragma unroll
   for (int mb = 0; mb < RM; ++mb) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float s = 0.f;
 #pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb) s = fmaf(acc[mb][nb][i], acc[mb][nb][i], s);
+      for (int nb = 0; nb < NB; ++nb) s = fmaf(acc[mb][nb][i], acc[mb][nb][i], s);
       s += __shfl_xor(s, 1, kWave);
       s += __shfl_xor(s, 2, kWave);
       s += __shfl_xor(s, 4, kWave);

@@ -90,8 +90,8 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   const size_t slice = (size_t)nbp * 1024;
   const unsigned char* wf =
       frags + (size_t)side * dkp * 3 * slice + (size_t)wave * kNbPerWave * 1024 + lane * 16;
-  BFrag b0;
-  load_bfrag(b0, wf, slice, 0);  // in flight during the gather
+  BFrag<kNbPerWave> b0;
+  load_bfrag<kNbPerWave>(b0, wf, slice, 0);  // in flight during the gather
 
   // gather the embedding rows (zero rows past M or for ids outside [0, V); zero k-padding)
   for (int r = tid; r < ROWS; r += nthreads) {
@@ -104,8 +104,8 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   __syncthreads();
 
   f32x4 acc[RM][kNbPerWave];
-  project_tile<RM>(acc, b0, A, astride, wf, slice, dkp, lane);
-  row_sumsq<RM>(acc, ssbuf + wave * ROWS, lane);
+  project_tile<RM, kNbPerWave>(acc, b0, A, astride, wf, slice, dkp, lane);
+  row_sumsq<RM, kNbPerWave>(acc, ssbuf + wave * ROWS, lane);
   __syncthreads();
   float* out = side == 0 ? in_vec : out_vec;
   const int col0 = wave * kNbPerWave * 16 + (lane & 15);

@@ -86,17 +86,17 @@ def test_scorer_matches_oracle(lib, sc, mode):
     _check(g, r, mode, f"{mode} {sc}")
 
 
-def test_scorer_headline_sampled(lib):
-    """The headline shape (64 requests of 15 x 16 candidates, width 1024, two layers) in one call;
-    requests are independent, so the oracle checks a sample of them on its own."""
+def test_scorer_headline_all_requests(lib):
+    """The headline shape (64 requests of 15 x 16 candidates, width 1024, two layers) in one call,
+    every request checked against the oracle (run eight requests at a time)."""
     sc = workloads.SCORER_HEADLINE
     print(f"scorer headline {sc}", flush=True)
     inp = workloads.make_scorer_inputs(sc)
     g = _gpu(lib, inp["X"], inp["layers"], sc)
     ol = _oracle_layers(inp["layers"])
-    for n in (0, 21, 42, 63):
-        r = osc.scorer_forward(inp["X"][n:n + 1].numpy(), ol, sc.S, sc.K, sc.heads)
-        _check(g[n:n + 1], r, "full", f"headline request {n}")
+    r = np.concatenate([osc.scorer_forward(inp["X"][n:n + 8].numpy(), ol, sc.S, sc.K, sc.heads)
+                        for n in range(0, sc.N, 8)])
+    _check(g, r, "full", "headline, all 64 requests")
 
 
 def test_scorer_plumbing_exact(lib):
