@@ -296,6 +296,16 @@ def scorer_rate(L, torch, workloads, iters=50, warmup=10):
             "frac_of_bf16_peak": flops / us / 1e6 / PEAK_BF16_TFLOPS}
 
 
+def calibration_copies(torch):
+    """Three plain 1 GiB device copies: under rocprofv3 --pmc they calibrate what FETCH_SIZE and
+    WRITE_SIZE read for a known number of bytes."""
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def cpu_baseline(cfg, inp, seconds):
     """The oracle chain, single-threaded, on whole requests of the workload until `seconds`."""
     import numpy as np
@@ -386,9 +396,10 @@ def main():
 
     if args.workload_step:
         c = next(c for c in workloads.CONFIGS if c.name == args.workload_step)
-        print(json.dumps({"per_workload": {c.name: per_config_rates(L, torch, c,
-                                                                    workloads.make_inputs(c))}}),
-              flush=True)
+        line = {"per_workload": {c.name: per_config_rates(L, torch, c, workloads.make_inputs(c))}}
+        if args.calibrate_copy:
+            calibration_copies(torch)
+        print(json.dumps(line), flush=True)
         return
 
     if args.logits_only:
@@ -398,11 +409,7 @@ def main():
         t, lo, hi = time_logits_pass(L, torch, c, bufs, iters=100 if c.index == 3 else 20)
         nb = c.N * c.B * c.V * 2 + c.N * c.B * c.K * 8
         if args.calibrate_copy:
-            src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-            dst = torch.empty_like(src)
-            for _ in range(3):
-                dst.copy_(src)
-            torch.cuda.synchronize()
+            calibration_copies(torch)
         print(json.dumps({"logits_pass": c.name, "us": t * 1e6, "us_batch_min": lo * 1e6,
                           "us_batch_max": hi * 1e6, "GB_s": nb / t / 1e9,
                           "frac_of_8TBs": nb / t / 1e9 / PEAK_HBM_GBS,
@@ -636,11 +643,7 @@ def main():
         out["scorer"] = scorer_rate(L, torch, workloads)
 
     if args.calibrate_copy:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
+        calibration_copies(torch)
 
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, inp, args.cpu_seconds)

@@ -1,8 +1,11 @@
 """GPU parity of step 1 (lilicorr_topk) against the oracle: ids bit-exact, logp within 1e-5.
 
 Every row of every workload: configs 0-2 directly, configs 3-4 (full size, the benchmark's
-launch configuration) against the oracle chain of every request, computed on a thread pool. Edge cases: ragged and tiny vocabularies, K = 1 and K = 64,
-exact ties, signed zeros, -inf, rows split over several workgroups, fp32 and bf16 logits.
+launch configuration) against the oracle chain of every request, computed on a thread pool.
+Edge cases: ragged and tiny vocabularies, K = 1 and K = 64, exact ties, signed zeros, -inf, rows
+split over several workgroups, fp32 and bf16 logits. Also: forced expiry of the kernel's bounded
+waits (reported, never silent), bit-identical repeated calls, and the vocabulary-sharded layout
+(per-shard top-K merged on the host) against the unsharded result.
 """
 import numpy as np
 import pytest
@@ -213,3 +216,44 @@ def test_topk_logp_is_deterministic(lib, cfg_inputs):
         b = [to_np(t) for t in lib.topk(x, cfg.K)]
         assert_equal(b[0], a[0], "ids of repeated calls")
         assert_equal(b[1], a[1], "logp of repeated calls")
+
+
+# ---- the vocabulary-sharded layout on one GPU ----------------------------------------------------
+
+def test_topk_vocabulary_shards_merge(lib, cfg_inputs, oracle_chain):
+    """What a tensor-parallel LM head over 8 GPUs would hand this path: each shard holds V/8 =
+    18,992 columns of every slot. Each shard's lilicorr_topk runs on its own slice; the exchange
+    the sharded design needs per slot is the shard's K (id + base, logit) keys and its
+    log-sum-exp (recovered here from the shard's top key: lse_shard = x[id_0] - logp_shard[0]).
+    Merged (keys by value desc, global id asc; lse = logsumexp over shards), they must equal the
+    unsharded result of the oracle chain: ids bit-exact, logp within tolerance."""
+    cfg, inp = cfg_inputs(3)
+    x = inp["logits"]  # [64, 16, 151936] bf16
+    N, B, V, K = cfg.N, cfg.B, cfg.V, cfg.K
+    P = 8
+    w = V // P
+    assert w * P == V
+    xb = to_np(x)  # bf16 bit patterns
+
+    def values(gid):  # the logits at global ids, widened exactly
+        bits = np.take_along_axis(xb, gid, axis=-1).astype(np.uint32) << 16
+        return bits.view(np.float32).astype(np.float64)
+
+    keys_v, keys_id, lses = [], [], []
+    for p in range(P):
+        sl = x[:, :, p * w:(p + 1) * w].contiguous()
+        gi, gl = _run(lib, sl, K)
+        gid = gi.astype(np.int64) + p * w
+        xv = values(gid)
+        keys_v.append(xv)
+        keys_id.append(gid)
+        lses.append(xv[..., 0] - gl[..., 0].astype(np.float64))
+    kv = np.concatenate(keys_v, -1)
+    ki = np.concatenate(keys_id, -1)
+    order = np.lexsort((ki, -kv), axis=-1)[..., :K]
+    ids = np.take_along_axis(ki, order, -1).astype(np.int32)
+    lse = np.logaddexp.reduce(np.stack(lses, -1), axis=-1)
+    logp = (np.take_along_axis(kv, order, -1) - lse[..., None]).astype(np.float32)
+    r = oracle_chain(3)
+    assert_equal(ids, r["ids"], "merged shard ids")
+    assert_close(logp, r["logp"], "merged shard logp")
