@@ -7,7 +7,10 @@
 // is handled by a group of 16, 32 or 64 lanes (one lane per candidate) with DPP butterflies, and
 // the results go to an LDS table. One lane then follows the table, one LDS read per slot, and the
 // whole workgroup writes the slots' outputs. One workgroup per request; slots are processed in
-// segments whose table fits in LDS.
+// segments whose table fits in LDS. Workgroups have 256 threads at K <= 16 (one round of row loads
+// covers a 16-slot block's 241 rows) and 512 above (at K = 32 the 481 rows take two rounds of
+// loads instead of four; 1024 threads would cap the registers below what 16 rows in flight per
+// lane need).
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -18,12 +21,14 @@
 namespace lilicorr {
 namespace {
 
-constexpr int kWalkThreads = 256;
+// threads per workgroup for groups of G lanes
+template <int G>
+__host__ __device__ constexpr int walk_threads() { return G <= 16 ? 256 : 512; }
 constexpr int kSegRows = 2048;  // table rows per segment (slots per segment: kSegRows / K)
 constexpr int kRowBatch = 16;   // rows per group whose loads are issued together
 
 template <int G>
-__global__ __launch_bounds__(kWalkThreads) void greedy_walk_kernel(
+__global__ __launch_bounds__(walk_threads<G>()) void greedy_walk_kernel(
     const float* __restrict__ S, const float* __restrict__ S0, const float* __restrict__ logp,
     const int32_t* __restrict__ ids, int64_t B, int K, float lambda,
     int32_t* __restrict__ draft, int32_t* __restrict__ choice, float* __restrict__ logq) {
@@ -32,6 +37,7 @@ __global__ __launch_bounds__(kWalkThreads) void greedy_walk_kernel(
   __shared__ int32_t seg_choice[kSegRows];
   __shared__ float seg_logq[kSegRows];
 
+  constexpr int kWalkThreads = walk_threads<G>();
   const int64_t n = blockIdx.x;
   const int tid = threadIdx.x;
   const int j = tid % G;                 // candidate index within the row
@@ -116,15 +122,15 @@ extern "C" lilicorr_status lilicorr_greedy_walk(const float* S, const float* S0,
   if ((S && !aligned16(S)) || (S0 && !aligned16(S0)) || !aligned16(logp) || !aligned16(ids) ||
       !aligned16(draft) || (choice && !aligned16(choice)) || (logq && !aligned16(logq)))
     return LILICORR_ERR_ALIGNMENT;
-  const dim3 grid((unsigned)N), block(kWalkThreads);
+  const dim3 grid((unsigned)N);
   if (K <= 16)
-    hipLaunchKernelGGL(greedy_walk_kernel<16>, grid, block, 0, stream, S, S0, logp, ids, B, K,
-                       logp_weight, draft, choice, logq);
+    hipLaunchKernelGGL(greedy_walk_kernel<16>, grid, dim3(walk_threads<16>()), 0, stream, S, S0,
+                       logp, ids, B, K, logp_weight, draft, choice, logq);
   else if (K <= 32)
-    hipLaunchKernelGGL(greedy_walk_kernel<32>, grid, block, 0, stream, S, S0, logp, ids, B, K,
-                       logp_weight, draft, choice, logq);
+    hipLaunchKernelGGL(greedy_walk_kernel<32>, grid, dim3(walk_threads<32>()), 0, stream, S, S0,
+                       logp, ids, B, K, logp_weight, draft, choice, logq);
   else
-    hipLaunchKernelGGL(greedy_walk_kernel<64>, grid, block, 0, stream, S, S0, logp, ids, B, K,
-                       logp_weight, draft, choice, logq);
+    hipLaunchKernelGGL(greedy_walk_kernel<64>, grid, dim3(walk_threads<64>()), 0, stream, S, S0,
+                       logp, ids, B, K, logp_weight, draft, choice, logq);
   return launch_status();
 }
