@@ -121,7 +121,7 @@ lilicorr_status lilicorr_topk_features(const void *logits, lilicorr_dtype dtype,
  *   packed    device buffer of lilicorr_packed_weight_bytes(d) bytes, owned by the caller.
  *
  * lilicorr_candidate_vectors
- *   ids       [N][B][K] int32 (as produced by step 1).
+ *   ids       [N][B][K] int32 (as produced by step 1); an id outside [0, V) gives zero vectors.
  *   E         [V][d] embedding table in `e_dtype` (bf16 uses matrix cores; fp32 uses vector FMA).
  *   packed_w  buffer filled by lilicorr_pack_weights for the same d.
  *   in_vec, out_vec  [N][B][K][d] fp32 out.

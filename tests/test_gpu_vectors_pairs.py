@@ -68,6 +68,37 @@ def test_vectors_shapes(lib, d, K, N, B, e_dtype):
     assert (giv.reshape(-1, d)[0] == 0).all()
 
 
+@pytest.mark.parametrize("d", [512, 496])
+def test_vectors_persistent_tiles(lib, d):
+    """Enough 64-row tiles at 480 < d <= 512 (1280 tiles, a ragged last tile of 24 rows) for the
+    persistent kernel that overlaps the next tile's row copies with the current tile's products.
+    d = 496 leaves the last two 16-byte lanes of every row copy outside the row. Ids outside
+    [0, V) give zero vectors; the oracle takes the in-range rows."""
+    N, B, K, V = 40, 31, 33, 3000
+    print(f"vectors persistent d={d} M={N * B * K}", flush=True)
+    rng = np.random.default_rng(d)
+    E32 = (rng.standard_normal((V, d)) * 0.05).astype(np.float32)
+    E32[7] = 0.0
+    W_in = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
+    W_out = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
+    ids = rng.integers(0, V, size=(N, B, K)).astype(np.int32)
+    M = N * B * K
+    flat = ids.reshape(M)
+    flat[0], flat[M - 1], flat[5000], flat[M - 30] = 7, 7, -1, V
+    E = torch.from_numpy(E32).to(torch.bfloat16)
+    giv, gov = _gpu_vectors(lib, ids, E, torch.from_numpy(W_in), torch.from_numpy(W_out))
+    giv, gov = giv.reshape(M, d), gov.reshape(M, d)
+    for r in (5000, M - 30):
+        assert (giv[r] == 0).all() and (gov[r] == 0).all(), f"row {r} of an out-of-range id"
+    sample = np.unique(np.concatenate([np.arange(64), np.arange(M - 64, M),
+                                       rng.choice(M, 700, replace=False)]))
+    sample = sample[(flat[sample] >= 0) & (flat[sample] < V)]
+    riv, rov = oracle.candidate_vectors(flat[sample][None, None], to_np(E), W_in, W_out)
+    assert_close(giv[sample], riv.reshape(-1, d), f"d={d} in_vec")
+    assert_close(gov[sample], rov.reshape(-1, d), f"d={d} out_vec")
+    assert (giv[0] == 0).all() and (giv[M - 1] == 0).all()
+
+
 def test_vectors_identity_weights(lib):
     d, V = 64, 50
     rng = np.random.default_rng(9)
