@@ -135,23 +135,24 @@ def stream_reader(torch):
     return read
 
 
-def stream_read_rate(torch, bufs, iters=20, warmup=3):
-    """GB/s of the plain streaming read over the same resident buffers, rotated like the logits
-    pass reads them: the read ceiling the logits pass is compared with."""
+def stream_read_rate(torch, bufs, iters=20, batches=3):
+    """GB/s of the plain streaming read over the same resident buffers, rotated and timed like the
+    logits pass (batches of `iters` back-to-back launches between two HIP events, after one
+    untimed batch; the mean per-launch time): the read ceiling the logits pass is compared with."""
     read = stream_reader(torch)
-    run = lambda i: read(bufs[i % len(bufs)])
 
-    for i in range(warmup):
-        run(i)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(iters)]
-    torch.cuda.synchronize()
-    for i in range(iters):
-        ev[i][0].record()
-        run(i)
-        ev[i][1].record()
-    torch.cuda.synchronize()
-    sec = statistics.mean(a.elapsed_time(b) for a, b in ev) / 1e3
+    def batch():
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(iters):
+            read(bufs[i % len(bufs)])
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 1e3 / iters
+
+    batch()
+    sec = statistics.mean(batch() for _ in range(batches))
     nbytes = bufs[0].numel() * bufs[0].element_size()
     return nbytes / sec / 1e9
 
@@ -508,11 +509,45 @@ def main():
     for i in range(args.warmup):
         step_separate(i)
     sep_elapsed = timed(step_separate, args.steps)
+    # Consecutive blocks of independent request batches alternate between two streams (default
+    # priority), each with its own outputs and workspaces: one block's correlation pass can run
+    # beside the next block's logits pass. Drafts are checked against the one-stream result.
+    s2 = torch.cuda.Stream()
+    ids2, logp2 = torch.empty_like(ids), torch.empty_like(logp)
+    ws2 = L.topk_workspace(N, B, V, K)
+    ws_fused2 = L.score_walk_workspace(N, B, K)
+    draft2, choice2, logq2 = torch.empty_like(draft), torch.empty_like(choice), torch.empty_like(logq)
+    topk_args2 = [(lg.data_ptr(), L.BF16, N, B, V, K, ids2.data_ptr(), logp2.data_ptr(),
+                   ws2.data_ptr(), ws2.numel(), s2.cuda_stream) for lg in logits_list]
+    walk_args2 = ((ids2.data_ptr(), logp2.data_ptr()) + walk_args[2:15] +
+                  (draft2.data_ptr(), choice2.data_ptr(), logq2.data_ptr(), ws_fused2.data_ptr(),
+                   ws_fused2.numel(), s2.cuda_stream))
+
+    def step_two_streams(i):
+        if i % 2 == 0:
+            step(i)
+        elif c_topk(*topk_args2[i % ROTATE]) != 0 or c_walk(*walk_args2) != 0:
+            raise RuntimeError("step failed")
+
+    torch.cuda.synchronize()
+    for i in range(args.warmup):
+        step_two_streams(i)
+    two_elapsed = timed(step_two_streams, args.steps)
+    expect = []
+    for b in range(2):
+        step(b)
+        torch.cuda.synchronize()
+        expect.append(draft.clone())
+    step_two_streams(0)
+    step_two_streams(1)
+    torch.cuda.synchronize()
+    if not (torch.equal(draft, expect[0]) and torch.equal(draft2, expect[1])):
+        raise RuntimeError("two-stream drafts differ from the one-stream drafts")
     print(f"[bench] timed {args.steps} steps in {elapsed:.4f} s (graph replay: "
-          f"{graph_elapsed:.4f} s, separate calls: {sep_elapsed:.4f} s)", file=sys.stderr,
-          flush=True)
-    if L.topk_wait_status(ws) != 0 or any(L.topk_wait_status(gr.topk_workspace) != 0
-                                          for gr in graphs):
+          f"{graph_elapsed:.4f} s, separate calls: {sep_elapsed:.4f} s, two streams: "
+          f"{two_elapsed:.4f} s)", file=sys.stderr, flush=True)
+    if L.topk_wait_status(ws) != 0 or L.topk_wait_status(ws2) != 0 or any(
+            L.topk_wait_status(gr.topk_workspace) != 0 for gr in graphs):
         raise RuntimeError("a bounded wait of the logits pass gave up: outputs invalid")
     for gr in graphs:
         gr.close()
@@ -553,6 +588,10 @@ def main():
                                  "lilicorr_block_graph_launch per block",
                          "ms_per_step": graph_elapsed / args.steps * 1e3,
                          "value": N * args.steps / graph_elapsed},
+        "two_streams": {"path": "the timed step's two C-ABI calls, consecutive blocks "
+                                "alternating between two streams with their own buffers",
+                        "ms_per_step": two_elapsed / args.steps * 1e3,
+                        "value": N * args.steps / two_elapsed},
         "separate_calls": {"path": "topk -> candidate_vectors -> pair_scores -> greedy_walk",
                            "ms_per_step": sep_elapsed / args.steps * 1e3,
                            "value": N * args.steps / sep_elapsed},
@@ -601,7 +640,7 @@ def main():
             logits_list[0], K, out=(ids, logp, feat), workspace=ws, features=True))
         plain_us = median_launch_us(torch, lambda: L.topk(logits_list[0], K, out=(ids, logp),
                                                           workspace=ws))
-        read3 = stream_read_rate(torch, logits_list)
+        read3 = stream_read_rate(torch, logits_list, iters=100)
         logits_list = None
         torch.cuda.empty_cache()
         t4, lo4, hi4 = time_logits_pass(L, torch, c4, [lg4], iters=20)
@@ -615,11 +654,13 @@ def main():
                          "us_batch_min": lo3 * 1e6, "us_batch_max": hi3 * 1e6,
                          "frac_of_8TBs": algo_bytes / t3 / 1e9 / PEAK_HBM_GBS,
                          "stream_read_GB_s": read3,
+                         "frac_of_stream_read": algo_bytes / t3 / 1e9 / read3,
                          "with_features_us_median": feat_us, "same_buffer_us_median": plain_us},
             "stress": {"GB_s": b4 / t4 / 1e9, "us": t4 * 1e6,
                        "us_batch_min": lo4 * 1e6, "us_batch_max": hi4 * 1e6,
                        "frac_of_8TBs": b4 / t4 / 1e9 / PEAK_HBM_GBS,
                        "stream_read_GB_s": read4,
+                       "frac_of_stream_read": b4 / t4 / 1e9 / read4,
                        "workload": "N=256, B=16, K=32, V=262144, bf16 logits"},
         }
         del lg4
