@@ -53,6 +53,8 @@ def parse():
                     help="skip the scoring-Transformer stand-in line")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-workload line (both metrics at every workload)")
+    ap.add_argument("--no-two-streams", action="store_true",
+                    help="skip the two-stream timing (profiling runs of the one-stream kernels)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
     ap.add_argument("--workload-step", choices=["tiny", "single", "tiers16", "headline64",
@@ -529,23 +531,26 @@ def main():
         elif c_topk(*topk_args2[i % ROTATE]) != 0 or c_walk(*walk_args2) != 0:
             raise RuntimeError("step failed")
 
-    torch.cuda.synchronize()
-    for i in range(args.warmup):
-        step_two_streams(i)
-    two_elapsed = timed(step_two_streams, args.steps)
-    expect = []
-    for b in range(2):
-        step(b)
+    two_elapsed = None
+    if not args.no_two_streams:
         torch.cuda.synchronize()
-        expect.append(draft.clone())
-    step_two_streams(0)
-    step_two_streams(1)
-    torch.cuda.synchronize()
-    if not (torch.equal(draft, expect[0]) and torch.equal(draft2, expect[1])):
-        raise RuntimeError("two-stream drafts differ from the one-stream drafts")
+        for i in range(args.warmup):
+            step_two_streams(i)
+        two_elapsed = timed(step_two_streams, args.steps)
+        expect = []
+        for b in range(2):
+            step(b)
+            torch.cuda.synchronize()
+            expect.append(draft.clone())
+        step_two_streams(0)
+        step_two_streams(1)
+        torch.cuda.synchronize()
+        if not (torch.equal(draft, expect[0]) and torch.equal(draft2, expect[1])):
+            raise RuntimeError("two-stream drafts differ from the one-stream drafts")
+    two_note = "" if two_elapsed is None else f", two streams: {two_elapsed:.4f} s"
     print(f"[bench] timed {args.steps} steps in {elapsed:.4f} s (graph replay: "
-          f"{graph_elapsed:.4f} s, separate calls: {sep_elapsed:.4f} s, two streams: "
-          f"{two_elapsed:.4f} s)", file=sys.stderr, flush=True)
+          f"{graph_elapsed:.4f} s, separate calls: {sep_elapsed:.4f} s{two_note})",
+          file=sys.stderr, flush=True)
     if L.topk_wait_status(ws) != 0 or L.topk_wait_status(ws2) != 0 or any(
             L.topk_wait_status(gr.topk_workspace) != 0 for gr in graphs):
         raise RuntimeError("a bounded wait of the logits pass gave up: outputs invalid")
@@ -588,10 +593,11 @@ def main():
                                  "lilicorr_block_graph_launch per block",
                          "ms_per_step": graph_elapsed / args.steps * 1e3,
                          "value": N * args.steps / graph_elapsed},
-        "two_streams": {"path": "the timed step's two C-ABI calls, consecutive blocks "
-                                "alternating between two streams with their own buffers",
-                        "ms_per_step": two_elapsed / args.steps * 1e3,
-                        "value": N * args.steps / two_elapsed},
+        "two_streams": None if two_elapsed is None else {
+            "path": "the timed step's two C-ABI calls, consecutive blocks alternating between "
+                    "two streams with their own buffers",
+            "ms_per_step": two_elapsed / args.steps * 1e3,
+            "value": N * args.steps / two_elapsed},
         "separate_calls": {"path": "topk -> candidate_vectors -> pair_scores -> greedy_walk",
                            "ms_per_step": sep_elapsed / args.steps * 1e3,
                            "value": N * args.steps / sep_elapsed},
