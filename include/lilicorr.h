@@ -353,9 +353,9 @@ void lilicorr_block_graph_destroy(lilicorr_graph *graph);
  * appendix, "Architecture"; widths and depth from the hyper-parameter table): a stack of
  * bidirectional Transformer layers over each request's candidate lattice of S slots x K
  * candidates (L = S * K nodes, node j in slot j / K), width H, H / 128 heads of width 128,
- * feed-forward width F, RMSNorm and SiLU, with two learned per-head attention biases added to the
- * attention logits: one indexed by the signed slot distance (query slot - key slot), one added
- * when both nodes share a slot. Each layer is pre-norm:
+ * feed-forward width F, RMSNorm and SiLU. Node order enters only through per-head scalars
+ * summed into the pre-softmax scores: a table looked up by (query slot - key slot), and one value
+ * for pairs of nodes in the same slot. Each layer is pre-norm:
  *     x += Wo . attn(rmsnorm(x; g_attn));   x += W2 . silu(W1 . rmsnorm(x; g_ffn))
  * with rmsnorm(x; g) = x / sqrt(mean(x^2) + 1e-6) * g, attention logits scaled by 1/sqrt(128),
  * every node attending to every node of its request. A cost-only stand-in: the weights are the

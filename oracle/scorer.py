@@ -6,9 +6,9 @@ CPU-baseline leg; the product path never imports it. It shares no code with the 
 What is computed (implementation appendix, "Architecture"; hyper-parameter table): a stack of
 bidirectional Transformer layers over one request's candidate lattice of S slots x K candidates
 (L = S * K nodes, node j in slot j // K), hidden width H, `heads` attention heads of width
-H / heads, feed-forward width F, RMSNorm and SiLU. Position enters through two learned per-head
-attention biases added to the attention logits: one indexed by the signed slot distance of the
-pair (query slot minus key slot), one added when both nodes occupy the same slot.
+H / heads, feed-forward width F, RMSNorm and SiLU. Node order enters only through per-head
+scalars summed into the pre-softmax scores: a table looked up by (query slot - key slot), and one
+value for pairs of nodes in the same slot.
 
 Readings of what the paper leaves open (each listed in the design notes):
   * pre-norm residual blocks: x += Wo . attn(rmsnorm(x; g_attn)); x += W2 . silu(W1 . rmsnorm(x;
