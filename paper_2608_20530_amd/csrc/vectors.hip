@@ -263,6 +263,257 @@ __global__ __launch_bounds__(512) void cand_vectors_stream_kernel(
   }
 }
 
+// Wide persistent variant for many tiles at 448 < d <= 512 (32 k-blocks of the contraction, 32
+// column blocks). The weight fragments stream from L2 once per tile and are reused by every row
+// of it, so the L2 read per row falls with the tile height; at 64 rows (two waves per SIMD, 256
+// registers each) the fragment read keeps pace with the matrix cores only just. Here a tile is
+// 128 rows and each of four waves (one per SIMD, so 512 registers: the 128 x 128 accumulator
+// block in the accumulation registers) owns 128 columns, which halves the L2 read per row.
+//  * The gathered tile (128 rows of bf16, both halves of the k range) lives in LDS as
+//    [half][row][256 bf16 + 8 of padding], so the 16 rows one fragment read touches fall in 16
+//    different bank groups and every k-block's reads sit at fixed offsets from one lane base.
+//  * Rows arrive by direct global-to-LDS loads, one half row per wave instruction (32 lanes),
+//    four per wave in every k-block: a tile's second half while its first half is multiplied,
+//    the next tile's first half while its second half is. The ids of a wave's 32 rows sit one
+//    per lane, so a copy reads no LDS in the k-loop.
+//  * The k-block loop is unrolled, so the accumulators stay in place across k-blocks, and the
+//    weight fragments come through a buffer descriptor with one lane offset (their k-block and
+//    term displacements are scalar), in pieces of two column blocks with three pieces in flight.
+//  * Nothing spills: a value reloaded from scratch in the output phase would make each 16-row
+//    block of stores wait for the previous block's to complete.
+//  * Products run with the weight fragment as the first operand, so each lane ends up holding
+//    four consecutive columns of one row: the unit vectors leave as 16-byte stores.
+// Tile t is side t % 2 (0: W_in), rows (t / 2) * 128 onwards.
+constexpr int kWideRows = 128;
+constexpr int kWideWaves = 4;
+constexpr int kWideNb = 8;      // 16-column blocks per wave
+constexpr int kWideDkp = 16;    // 32-deep k-blocks
+constexpr int kHalfChunks = 32; // 16-byte chunks per half row (256 bf16)
+constexpr int kHalfStride = kHalfChunks * 16 + 16;  // bytes per half row in LDS (padded)
+constexpr size_t kWideHalfBytes = (size_t)kWideRows * kHalfStride;
+
+// B fragments of one piece through a buffer descriptor: one lane offset, the k-block and term
+// displacements in the scalar offset, the column-block steps in the instruction offset
+template <int NBP>
+__device__ __forceinline__ void wide_bpiece(BFrag<NBP>& dst, __amdgpu_buffer_rsrc_t rs,
+                                            uint32_t voff, uint32_t sbase, uint32_t slice, int kb) {
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const uint32_t so = sbase + (uint32_t)(kb * 3 + t) * slice;
+#pragma unroll
+    for (int j = 0; j < NBP; ++j)
+      dst[j][t] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff + (uint32_t)j * 1024u, so, 0));
+  }
+}
+
+// acc[mb][NBP g + j] += W-fragment x E-fragment over one k-block for column blocks NBP g ..
+template <int NBP>
+__device__ __forceinline__ void wide_mfma(f32x4 (&acc)[8][kWideNb], const BFrag<NBP>& b,
+                                          const bf16x8 (&a)[8], int g) {
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+      for (int j = 0; j < NBP; ++j)
+        acc[mb][NBP * g + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, b[j][t]), a[mb], acc[mb][NBP * g + j], 0, 0, 0);
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* __restrict__ E,
+                              const unsigned char* __restrict__ frags, int64_t M, int64_t V,
+                              int d, int nbp, int64_t ntiles, float* __restrict__ in_vec,
+                              float* __restrict__ out_vec) {
+  constexpr int ROWS = kWideRows, NW = kWideWaves;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, lane = lane_id(),
+            wave = (int)__builtin_amdgcn_readfirstlane((uint32_t)(tid / kWave));
+  unsigned char* A = smem;                                                // [2][ROWS][32][16 B]
+  float* ssbuf = reinterpret_cast<float*>(smem + 2 * kWideHalfBytes);    // [NW][ROWS]
+  int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + NW * ROWS);          // [2][ROWS]
+  const size_t slice = (size_t)nbp * 1024;
+  const int64_t step = gridDim.x;
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(E), (short)0, (int)(V * d * 2), 0x00020000);
+  const uint32_t kOut = 0x80000000u;
+  const int dchunks = d / 8;
+  const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<unsigned char*>(frags), (short)0, (int)(2 * kWideDkp * 3 * slice), 0x00020000);  // 16-byte chunks per embedding row (d % 16 == 0)
+
+  auto tile_id = [&](int64_t t) -> int32_t {
+    int32_t v = -1;
+    if (t < ntiles && tid < ROWS) {
+      const int64_t row = (t >> 1) * ROWS + tid;
+      if (row < M) {
+        const int32_t id = ids[row];
+        v = (id >= 0 && id < V) ? id : -1;
+      }
+    }
+    return v;
+  };
+  // half h of row `row` of the tile whose ids are in rr: lanes 0..31, one 16-byte chunk each
+  // (the row number passes through an empty asm so the compiler computes each copy's addresses
+  // where the copy is issued instead of hoisting all of them out of the tile loop into registers)
+  auto dma_half_id = [&](int32_t id, int h, int row) {
+    __asm__ volatile("" : "+s"(row));
+    if (lane < kHalfChunks) {
+      const int c = h * kHalfChunks + lane;
+      const uint32_t off =
+          (id >= 0 && c < dchunks) ? (uint32_t)id * (uint32_t)(d * 2) + (uint32_t)c * 16u : kOut;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsrc, (lds_ptr_t)(A + h * kWideHalfBytes + (size_t)row * kHalfStride), 16, off, 0, 0, 0);
+    }
+  };
+  auto dma_half = [&](const int32_t* rr, int h, int row) {
+    dma_half_id(__builtin_amdgcn_readfirstlane(rr[row]), h, row);
+  };
+
+  int64_t t = blockIdx.x;
+  {
+    const int32_t v0 = tile_id(t), v1 = tile_id(t + step);
+    if (tid < ROWS) {
+      rid[tid] = v0;
+      rid[ROWS + tid] = v1;
+    }
+  }
+  __syncthreads();
+  // the first tile's first half; its second half arrives during its first k-blocks
+  for (int r = wave; r < ROWS; r += NW) dma_half(rid, 0, r);
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int it = 0; t < ntiles; ++it, t += step) {
+    const int cur = it & 1, nxt = cur ^ 1;
+    const bool has_next = t + step < ntiles;
+    const int32_t* rc = rid + cur * ROWS;
+    const int32_t* rn = rid + nxt * ROWS;
+    const int side = (int)(t & 1);
+    const uint32_t sbase = (uint32_t)(side * kWideDkp * 3) * (uint32_t)slice;
+    const uint32_t voff = (uint32_t)(wave * kWideNb * 1024 + lane * 16);
+    const int32_t id_after = tile_id(t + 2 * step);  // written to rid[cur] at the end
+    // ids of the rows this wave copies, lane j holding row wave + 4 j (j < 32): this tile's (for
+    // its second half) and the next tile's (for its first half), read once so that a copy needs
+    // no LDS read in the k-loop
+    const int32_t idc = rc[(wave + NW * (lane & 31)) & (ROWS - 1)];
+    const int32_t idn = rn[(wave + NW * (lane & 31)) & (ROWS - 1)];
+
+    f32x4 acc[8][kWideNb];
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kWideNb; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the weight fragments of a k-block come in pieces of kPieceNb column blocks through
+    // kBufs register buffers: while a piece is multiplied the next kBufs - 1 are in flight
+    constexpr int kPieceNb = 2, kPieces = kWideNb / kPieceNb, kBufs = 4;
+    constexpr int kTotalPieces = kWideDkp * kPieces;
+    BFrag<kPieceNb> bq[kBufs];
+    auto load_piece = [&](int p) {
+      wide_bpiece<kPieceNb>(bq[p % kBufs], frs, voff + (uint32_t)((p % kPieces) * kPieceNb * 1024),
+                            sbase, (uint32_t)slice, p / kPieces);
+    };
+#pragma unroll
+    for (int p = 0; p < kBufs - 1; ++p) load_piece(p);
+    const int arow = lane & 15, agrp = lane >> 4;
+    // k-blocks kb0 .. kb0+7 from LDS half h. Four half-row copies per k-block go into the other
+    // half: this tile's second half while the first is multiplied (that half was released at
+    // the previous tile's end), the next tile's first half while the second is multiplied.
+    auto kloop = [&](int kb0, int h) {
+      const unsigned char* Ah = A + h * kWideHalfBytes;
+#pragma unroll
+      for (int kb = kb0; kb < kb0 + 8; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (h == 0) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int j = 4 * (kb - kb0) + i;
+            dma_half_id(__builtin_amdgcn_readlane(idc, j), 1, wave + NW * j);
+          }
+        } else if (has_next) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int j = 4 * (kb - kb0) + i;
+            dma_half_id(__builtin_amdgcn_readlane(idn, j), 0, wave + NW * j);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 a[8];
+        const unsigned char* Ak = Ah + arow * kHalfStride + ((kb & 7) * 4 + agrp) * 16;
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb)
+          a[mb] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4*>(Ak + mb * 16 * kHalfStride));
+#pragma unroll
+        for (int g = 0; g < kPieces; ++g) {
+          const int p = kb * kPieces + g;
+          if (p + kBufs - 1 < kTotalPieces) load_piece(p + kBufs - 1);
+          __builtin_amdgcn_sched_barrier(0);
+          wide_mfma<kPieceNb>(acc, bq[p % kBufs], a, g);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    };
+    kloop(0, 0);
+    // every wave is done with the first half, and the second half has landed: this wave's
+    // copies, then everyone's
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    kloop(8, 1);
+
+    // this wave's 128-column part of every row's squared norm: lane l holds row 16 mb + l % 16,
+    // columns 16 nb + 4 (l / 16) + i
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      float s = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < kWideNb; ++nb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s = fmaf(acc[mb][nb][i], acc[mb][nb][i], s);
+      s += __shfl_xor(s, 16, kWave);
+      s += __shfl_xor(s, 32, kWave);
+      if (lane < 16) ssbuf[wave * ROWS + mb * 16 + lane] = s;
+    }
+    // keep the accumulators in the accumulation registers between the two passes over them
+    // (copied into ordinary registers, they crowd out everything else and force spills)
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kWideNb; ++nb) __asm__ volatile("" : "+a"(acc[mb][nb]));
+    if (tid < ROWS) rid[cur * ROWS + tid] = id_after;
+    // the next tile's first half has landed and nobody reads this tile's second half any more
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+
+    float* out = side == 0 ? in_vec : out_vec;
+    const int64_t row0 = (t >> 1) * ROWS;
+    // the lane's row and column group, recomputed here (through an empty asm) rather than kept
+    // in registers from the top of the kernel: a value reloaded from scratch between the stores
+    // would make each 16-row block wait for the previous block's stores to complete
+    int le = lane;
+    __asm__ volatile("" : "+v"(le));
+    const int er = le & 15, eg = le >> 4;
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const int rl = mb * 16 + er;
+      float tot = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) tot += ssbuf[w * ROWS + rl];
+      const float inv = tot > 0.f ? 1.0f / sqrtf(tot) : 0.f;
+      const int64_t r = row0 + rl;
+      if (r < M) {
+#pragma unroll
+        for (int nb = 0; nb < kWideNb; ++nb) {
+          const int col = wave * kWideNb * 16 + nb * 16 + eg * 4;
+          if (col < d)
+            __builtin_nontemporal_store(acc[mb][nb] * inv,
+                                        reinterpret_cast<f32x4*>(&out[r * d + col]));
+        }
+      }
+    }
+  }
+}
+
 // Workgroups that run at once (one per compute unit), per device
 int compute_units() {
   static int cached[64] = {0};
@@ -402,9 +653,26 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
     const int64_t rows_wg = (int64_t)g.rm * 16;
     const int64_t nblk = (M + rows_wg - 1) / rows_wg;
     if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
+    const int ncu = compute_units();
+    // many 128-row tiles at 448 < d <= 512: the wide persistent kernel
+    if (g.dkp == kWideDkp && g.nbp == kWideWaves * kWideNb && ncu > 0 &&
+        2 * ((M + kWideRows - 1) / kWideRows) >= 4 * (int64_t)ncu &&
+        V * d * 2 < ((int64_t)1 << 31)) {
+      const int64_t wt = 2 * ((M + kWideRows - 1) / kWideRows);
+      const int grid = (int)(wt < ncu ? wt : ncu);
+      const size_t lds = 2 * kWideHalfBytes + (size_t)kWideWaves * kWideRows * sizeof(float) +
+                         (size_t)2 * kWideRows * sizeof(int32_t);
+      static const hipError_t attrw = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(cand_vectors_wide_kernel),
+          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      (void)attrw;
+      hipLaunchKernelGGL(cand_vectors_wide_kernel, dim3((unsigned)grid), dim3(kWideWaves * kWave),
+                         lds, stream, ids, static_cast<const uint16_t*>(E), p, M, V, d, g.nbp, wt,
+                         in_vec, out_vec);
+      return launch_status();
+    }
     // many 64-row tiles at 480 < d <= 512: the persistent kernel (at least four tiles per
     // compute unit; E addressable by a 32-bit buffer offset)
-    const int ncu = compute_units();
     const int64_t ntiles = 2 * nblk;
     if (g.rm == 4 && g.dkp == kStreamDkp && g.waves == 8 && d % 8 == 0 && ncu > 0 &&
         ntiles >= 4 * (int64_t)ncu && V * d * 2 < ((int64_t)1 << 31)) {

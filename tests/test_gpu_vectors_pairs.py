@@ -68,15 +68,17 @@ def test_vectors_shapes(lib, d, K, N, B, e_dtype):
     assert (giv.reshape(-1, d)[0] == 0).all()
 
 
-@pytest.mark.parametrize("d", [512, 496])
-def test_vectors_persistent_tiles(lib, d):
-    """Enough 64-row tiles at 480 < d <= 512 (1280 tiles, a ragged last tile of 24 rows) for the
-    persistent kernel that overlaps the next tile's row copies with the current tile's products.
-    d = 496 leaves the last two 16-byte lanes of every row copy outside the row. Ids outside
-    [0, V) give zero vectors; the oracle takes the in-range rows."""
-    N, B, K, V = 40, 31, 33, 3000
+@pytest.mark.parametrize("d,N,B,K", [(512, 40, 31, 33), (496, 40, 31, 33),
+                                     (512, 70, 31, 31), (464, 70, 31, 31)])
+def test_vectors_persistent_tiles(lib, d, N, B, K):
+    """The persistent kernels at 448 < d <= 512, which copy the next tile's rows into LDS while
+    the current tile's products run: 40 x 31 x 33 rows give 1280 tiles of 64 rows (a ragged last
+    tile of 24), 70 x 31 x 31 rows 1052 tiles of 128 (a ragged last tile of 70). d = 496 and 464
+    leave the end of every row copy outside the row. Ids outside [0, V) give zero vectors; the
+    oracle takes the in-range rows."""
+    V = 3000
     print(f"vectors persistent d={d} M={N * B * K}", flush=True)
-    rng = np.random.default_rng(d)
+    rng = np.random.default_rng(d + N)
     E32 = (rng.standard_normal((V, d)) * 0.05).astype(np.float32)
     E32[7] = 0.0
     W_in = (rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)
