@@ -174,12 +174,13 @@ def median_launch_us(torch, fn, iters=50, warmup=5):
     return statistics.median(a.elapsed_time(b) for a, b in ev) * 1e3
 
 
-def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
+def per_config_rates(L, torch, c, inp, iters=100, warmup=10, batches=10):
     """Both metrics at one workload: blocks/s of the step (logits pass, then the fused pass or the
     separate calls, through the C ABI with arguments marshalled once) and the logits pass's GB/s,
-    each the mean over `iters` back-to-back calls between two HIP events. The logits rotate over
-    enough resident copies (at least 1 GiB in all) that every call reads its logits from HBM, as in
-    the headline loop."""
+    each over `iters` back-to-back calls in `batches` batches between two HIP events (the mean,
+    and the median, p10 and p90 of the batch means), beside a plain streaming read of the same
+    logits buffers timed the same way. The logits rotate over enough resident copies (at least
+    1 GiB in all) that every call reads its logits from HBM, as in the headline loop."""
     lg = inp["logits"].cuda()
     nbytes = lg.numel() * lg.element_size()
     copies = max(1, min(1024, -(-(1 << 30) // nbytes)))
@@ -235,34 +236,44 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10):
             raise RuntimeError("lilicorr_topk failed")
 
     counter = [0]
+    per = max(1, iters // batches)
 
     def batch(fn):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         a.record()
-        for _ in range(iters):
+        for _ in range(per):
             fn(counter[0])
             counter[0] += 1
         b.record()
         torch.cuda.synchronize()
-        return a.elapsed_time(b) / 1e3 / iters
+        return a.elapsed_time(b) / 1e3 / per
+
+    def spread(ts):
+        q = sorted(ts)
+        return {"median_us": statistics.median(q) * 1e6, "p10_us": q[len(q) // 10] * 1e6,
+                "p90_us": q[min(len(q) - 1, (9 * len(q)) // 10)] * 1e6}
 
     for _ in range(warmup):
         topk(counter[0])
         rest()
         counter[0] += 1
-    step = batch(lambda i: (topk(i), rest()))
-    t_topk = batch(topk)
+    steps = [batch(lambda i: (topk(i), rest())) for _ in range(batches)]
+    topks = [batch(topk) for _ in range(batches)]
+    step, t_topk = statistics.mean(steps), statistics.mean(topks)
     if L.topk_wait_status(ws) != 0:
         raise RuntimeError("a bounded wait of the logits pass gave up: outputs invalid")
+    read = stream_read_rate(torch, lgs, iters=max(10, min(100, copies * 4)))
     return {"workload": f"{c.name}: N={N}, B={B}, K={K}, V={V}, d={c.d}, "
                         f"{'bf16' if lg.element_size() == 2 else 'fp32'} logits",
             "path": "lilicorr_topk -> " + ("lilicorr_score_walk" if fused else
                                             "candidate_vectors -> pair_scores -> greedy_walk"),
             "logits_copies": copies,
-            "blocks_s": N / step, "step_us": step * 1e6,
+            "blocks_s": N / step, "step_us": step * 1e6, "step_batches": spread(steps),
             "logits_GB_s": nbytes / t_topk / 1e9, "logits_us": t_topk * 1e6,
-            "logits_frac_of_8TBs": nbytes / t_topk / 1e9 / PEAK_HBM_GBS}
+            "logits_batches": spread(topks),
+            "logits_frac_of_8TBs": nbytes / t_topk / 1e9 / PEAK_HBM_GBS,
+            "stream_read_GB_s": read, "logits_frac_of_stream_read": nbytes / t_topk / 1e9 / read}
 
 
 PEAK_BF16_TFLOPS = 2500.0

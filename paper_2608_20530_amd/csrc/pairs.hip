@@ -179,11 +179,13 @@ extern "C" lilicorr_status lilicorr_pair_scores(const float* in_vec, const float
   const int npairs = (int)(B - 1) + (anchor_out ? 1 : 0);
   if (npairs == 0) return LILICORR_OK;
   const dim3 grid((unsigned)npairs, (unsigned)N);
-  // 16-row blocks per side: ceil(K / 16); chunk width 64 columns (32 for four blocks)
+  // 16-row blocks per side: ceil(K / 16); chunk width 64 columns at one block, 32 above (two
+  // chunks of 32 columns keep a wave under 128 registers, so the stress shape's 3840 matrices
+  // are all resident at once)
   if (K <= 16)
     launch_pairs<1, 4>(grid, stream, in_vec, out_vec, anchor_out, B, K, d, sigma, S, S0);
   else if (K <= 32)
-    launch_pairs<2, 4>(grid, stream, in_vec, out_vec, anchor_out, B, K, d, sigma, S, S0);
+    launch_pairs<2, 2>(grid, stream, in_vec, out_vec, anchor_out, B, K, d, sigma, S, S0);
   else
     launch_pairs<4, 2>(grid, stream, in_vec, out_vec, anchor_out, B, K, d, sigma, S, S0);
   return launch_status();
