@@ -195,15 +195,15 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10, batches=10):
     choice = torch.empty_like(draft)
     logq = torch.empty(N, B, dtype=torch.float32, device="cuda")
     # the fused pass holds both sides' fp32 projections in LDS (bf16 tables, d <= 256); other
-    # workloads take the separate calls. Every call goes straight to the C ABI with its arguments
-    # marshalled once, as in the headline loop.
+    # workloads take the candidate vectors, then pair scores and walk in one pass. Every call goes
+    # straight to the C ABI with its arguments marshalled once, as in the headline loop.
     lib = L.load_library()
     st = torch.cuda.current_stream().cuda_stream
     e_code = L.BF16 if E.dtype == torch.bfloat16 else L.F32
     l_code = L.BF16 if lg.dtype == torch.bfloat16 else L.F32
     fused = E.dtype == torch.bfloat16 and c.d <= 256
+    ws_fused = L.score_walk_workspace(N, B, K)
     if fused:
-        ws_fused = L.score_walk_workspace(N, B, K)
         walk_args = (ids.data_ptr(), logp.data_ptr(), E.data_ptr(), e_code, V, c.d,
                      packed.data_ptr(), None, N, B, K, L.SIGMA, 0.0, None, None, draft.data_ptr(),
                      choice.data_ptr(), logq.data_ptr(), ws_fused.data_ptr(), ws_fused.numel(), st)
@@ -214,19 +214,16 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10, batches=10):
     else:
         in_vec = torch.empty(N, B, K, c.d, dtype=torch.float32, device="cuda")
         out_vec = torch.empty_like(in_vec)
-        S = torch.empty(N, max(B - 1, 1), K, K, dtype=torch.float32, device="cuda")
         cv_args = (ids.data_ptr(), E.data_ptr(), e_code, V, c.d, packed.data_ptr(), N, B, K,
                    in_vec.data_ptr(), out_vec.data_ptr(), st)
-        ps_args = (in_vec.data_ptr(), out_vec.data_ptr(), None, N, B, K, c.d, L.SIGMA,
-                   S.data_ptr() if B > 1 else None, None, st)
-        gw_args = (S.data_ptr() if B > 1 else None, None, logp.data_ptr(), ids.data_ptr(), N, B,
-                   K, 0.0, draft.data_ptr(), choice.data_ptr(), logq.data_ptr(), st)
+        pw_args = (in_vec.data_ptr(), out_vec.data_ptr(), None, logp.data_ptr(), ids.data_ptr(), N,
+                   B, K, c.d, L.SIGMA, 0.0, None, None, draft.data_ptr(), choice.data_ptr(),
+                   logq.data_ptr(), ws_fused.data_ptr(), ws_fused.numel(), st)
 
         def rest():
             if (lib.lilicorr_candidate_vectors(*cv_args) != 0 or
-                    lib.lilicorr_pair_scores(*ps_args) != 0 or
-                    lib.lilicorr_greedy_walk(*gw_args) != 0):
-                raise RuntimeError("separate calls failed")
+                    lib.lilicorr_pair_walk(*pw_args) != 0):
+                raise RuntimeError("candidate_vectors -> pair_walk failed")
 
     tk_args = [(x.data_ptr(), l_code, N, B, V, K, ids.data_ptr(), logp.data_ptr(), ws.data_ptr(),
                 ws.numel(), st) for x in lgs]
@@ -267,7 +264,7 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10, batches=10):
     return {"workload": f"{c.name}: N={N}, B={B}, K={K}, V={V}, d={c.d}, "
                         f"{'bf16' if lg.element_size() == 2 else 'fp32'} logits",
             "path": "lilicorr_topk -> " + ("lilicorr_score_walk" if fused else
-                                            "candidate_vectors -> pair_scores -> greedy_walk"),
+                                            "lilicorr_candidate_vectors -> lilicorr_pair_walk"),
             "logits_copies": copies,
             "blocks_s": N / step, "step_us": step * 1e6, "step_batches": spread(steps),
             "logits_GB_s": nbytes / t_topk / 1e9, "logits_us": t_topk * 1e6,

@@ -292,6 +292,62 @@ lilicorr_status lilicorr_score_viterbi(const int32_t *ids, const float *logp, co
                                        hipStream_t stream);
 
 /*
+ * Steps 3-4 in one pass over the vectors of step 2, for any width lilicorr_candidate_vectors
+ * produces (Sec. 3.5: all pair matrices of the block in one batched pass, then the walk; the
+ * fused calls above hold both sides' vectors on chip, which bounds them to d <= 256). The draft,
+ * choice and logq are those lilicorr_pair_scores -> lilicorr_greedy_walk give on the same inputs,
+ * and S / S0 (when requested) are the same values, without S going to memory and back.
+ *   in_vec, out_vec  [N][B][K][d] fp32 from lilicorr_candidate_vectors; anchor_out [N][d] or NULL.
+ *   logp, ids        [N][B][K] from step 1.
+ *   sigma, logp_weight, S, S0, draft, choice, logq   as for lilicorr_score_walk.
+ *   workspace        lilicorr_score_walk_workspace_bytes(N, B, K) bytes, zero-filled once, with
+ *                    the rules of lilicorr_score_walk (calls sharing one must not overlap).
+ * Limits: K <= 64, 1 + (B-1) K <= 16384, N <= 65535, d a multiple of 16 and at most 1024
+ * (LILICORR_ERR_UNSUPPORTED otherwise; LILICORR_ERR_WORKSPACE if the workspace is too small).
+ */
+lilicorr_status lilicorr_pair_walk(const float *in_vec, const float *out_vec,
+                                   const float *anchor_out, const float *logp, const int32_t *ids,
+                                   int64_t N, int64_t B, int K, int d, float sigma,
+                                   float logp_weight, float *S, float *S0, int32_t *draft,
+                                   int32_t *choice, float *logq, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * lilicorr_pair_walk with certified decisions, as lilicorr_score_walk_certified defines them:
+ * a decision whose fp32 winner is within `margin` of another candidate is decided again from the
+ * embedding rows and the fp32 weights in double precision.
+ *   E, e_dtype, V, packed_w   the embedding table and packed weights the vectors were made from
+ *                             (bf16 E only; the fp32 weights come from the packed buffer's copy).
+ *   margin, rescored          as for lilicorr_score_walk_certified.
+ *   workspace                 lilicorr_score_walk_certified_workspace_bytes(N, B, K) bytes.
+ * Other arguments and limits as for lilicorr_pair_walk, with d at most 512.
+ */
+lilicorr_status lilicorr_pair_walk_certified(const float *in_vec, const float *out_vec,
+                                             const float *anchor_out, const float *logp,
+                                             const int32_t *ids, const void *E,
+                                             lilicorr_dtype e_dtype, int64_t V,
+                                             const void *packed_w, int64_t N, int64_t B, int K,
+                                             int d, float sigma, float logp_weight, float margin,
+                                             float *S, float *S0, int32_t *draft, int32_t *choice,
+                                             float *logq, int32_t *rescored, void *workspace,
+                                             size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The same pass with the exact max-path decode (decode-rule appendix): the draft, choice, logq and
+ * score that lilicorr_pair_scores -> lilicorr_viterbi_walk give on the same inputs. Arguments as
+ * for lilicorr_pair_walk plus score ([N] fp32 or NULL); workspace of
+ * lilicorr_score_viterbi_workspace_bytes(N, B, K) bytes. Limits: K <= 64, B <= 8192,
+ * B * K <= 65536, N <= 65535, d a multiple of 16 and at most 1024.
+ */
+lilicorr_status lilicorr_pair_viterbi(const float *in_vec, const float *out_vec,
+                                      const float *anchor_out, const float *logp,
+                                      const int32_t *ids, int64_t N, int64_t B, int K, int d,
+                                      float sigma, float logp_weight, float *S, float *S0,
+                                      int32_t *draft, int32_t *choice, float *logq, float *score,
+                                      void *workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/*
  * One draft block as one HIP graph (implementation appendix, serving: candidate extraction,
  * matching and selection replayed as one graph per block). lilicorr_block_graph_create records
  * lilicorr_topk followed by one fused pass (greedy, certified greedy or exact decode) with the

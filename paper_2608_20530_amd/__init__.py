@@ -119,6 +119,11 @@ def load_library() -> ctypes.CDLL:
         "lilicorr_score_viterbi_workspace_bytes": ([I64, I64, I], SZ),
         "lilicorr_score_viterbi": ([P, P, P, I, I64, I, P, P, I64, I64, I, F, F, P, P, P, P, P, P, P,
                                     SZ, P], I),
+        "lilicorr_pair_walk": ([P, P, P, P, P, I64, I64, I, I, F, F, P, P, P, P, P, P, SZ, P], I),
+        "lilicorr_pair_walk_certified": ([P, P, P, P, P, P, I, I64, P, I64, I64, I, I, F, F, F, P,
+                                          P, P, P, P, P, P, SZ, P], I),
+        "lilicorr_pair_viterbi": ([P, P, P, P, P, I64, I64, I, I, F, F, P, P, P, P, P, P, P, SZ,
+                                   P], I),
         "lilicorr_block_graph_create": ([ctypes.POINTER(BlockArgs), ctypes.POINTER(P)], I),
         "lilicorr_block_graph_launch": ([P, P], I),
         "lilicorr_block_graph_destroy": ([P], None),
@@ -244,6 +249,27 @@ def lilicorr_score_viterbi(ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N,
                            workspace_bytes, stream):
     return _call("lilicorr_score_viterbi", ids, logp, E, e_dtype, V, d, packed_w, anchor_out, N,
                  B, K, sigma, logp_weight, S, S0, draft, choice, logq, score, workspace,
+                 workspace_bytes, stream)
+
+
+def lilicorr_pair_walk(in_vec, out_vec, anchor_out, logp, ids, N, B, K, d, sigma, logp_weight, S,
+                       S0, draft, choice, logq, workspace, workspace_bytes, stream):
+    return _call("lilicorr_pair_walk", in_vec, out_vec, anchor_out, logp, ids, N, B, K, d, sigma,
+                 logp_weight, S, S0, draft, choice, logq, workspace, workspace_bytes, stream)
+
+
+def lilicorr_pair_walk_certified(in_vec, out_vec, anchor_out, logp, ids, E, e_dtype, V, packed_w,
+                                 N, B, K, d, sigma, logp_weight, margin, S, S0, draft, choice,
+                                 logq, rescored, workspace, workspace_bytes, stream):
+    return _call("lilicorr_pair_walk_certified", in_vec, out_vec, anchor_out, logp, ids, E,
+                 e_dtype, V, packed_w, N, B, K, d, sigma, logp_weight, margin, S, S0, draft,
+                 choice, logq, rescored, workspace, workspace_bytes, stream)
+
+
+def lilicorr_pair_viterbi(in_vec, out_vec, anchor_out, logp, ids, N, B, K, d, sigma, logp_weight,
+                          S, S0, draft, choice, logq, score, workspace, workspace_bytes, stream):
+    return _call("lilicorr_pair_viterbi", in_vec, out_vec, anchor_out, logp, ids, N, B, K, d,
+                 sigma, logp_weight, S, S0, draft, choice, logq, score, workspace,
                  workspace_bytes, stream)
 
 
@@ -527,6 +553,94 @@ def score_viterbi(ids: torch.Tensor, logp: torch.Tensor, E: torch.Tensor, packed
     if scores:
         return draft, choice, logq, score, S, S0
     return draft, choice, logq, score
+
+
+def _decode_outputs(N, B, K, dev, anchor_out, extra, scores, out):
+    """draft, choice, logq (+ the `extra` [N]-or-[N,B] output) and, with scores, S and S0."""
+    if out is None:
+        out = (torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.int32, device=dev),
+               torch.empty(N, B, dtype=torch.float32, device=dev))
+        if extra == "score":
+            out += (torch.empty(N, dtype=torch.float32, device=dev),)
+        elif extra == "rescored":
+            out += (torch.empty(N, B, dtype=torch.int32, device=dev),)
+    S = S0 = None
+    if scores:
+        S = torch.empty(N, max(B - 1, 0), K, K, dtype=torch.float32, device=dev)
+        S0 = torch.empty(N, K, dtype=torch.float32, device=dev) if anchor_out is not None else None
+    return tuple(out), S, S0
+
+
+def _vector_args(in_vec, out_vec, anchor_out, logp, ids):
+    N, B, K, d = in_vec.shape
+    if tuple(out_vec.shape) != (N, B, K, d) or tuple(ids.shape) != (N, B, K):
+        raise LilicorrError("in_vec, out_vec must be [N, B, K, d] and ids [N, B, K]")
+    return (N, B, K, d, _dev(in_vec, "in_vec", (torch.float32,)),
+            _dev(out_vec, "out_vec", (torch.float32,)),
+            _dev(anchor_out, "anchor_out", (torch.float32,)),
+            _dev(logp, "logp", (torch.float32,)), _dev(ids, "ids", (torch.int32,)))
+
+
+def pair_walk(in_vec: torch.Tensor, out_vec: torch.Tensor, logp: torch.Tensor, ids: torch.Tensor,
+              anchor_out=None, sigma: float = SIGMA, logp_weight: float = 0.0, *,
+              scores: bool = False, out=None, workspace=None):
+    """Steps 3-4 in one pass over the vectors of step 2 -> (draft, choice, logq[, S, S0 when
+    scores=True]); the workspace is score_walk's."""
+    N, B, K, d, *ptrs = _vector_args(in_vec, out_vec, anchor_out, logp, ids)
+    (draft, choice, logq), S, S0 = _decode_outputs(N, B, K, ids.device, anchor_out, None,
+                                                   scores, out)
+    if workspace is None:
+        workspace = score_walk_workspace(N, B, K, ids.device)
+    lilicorr_pair_walk(*ptrs, N, B, K, d, float(sigma), float(logp_weight),
+                       _dev(S, "S", (torch.float32,)) if S is not None and B > 1 else None,
+                       _dev(S0, "S0", (torch.float32,)), _dev(draft, "draft", (torch.int32,)),
+                       _dev(choice, "choice", (torch.int32,)), _dev(logq, "logq", (torch.float32,)),
+                       _dev(workspace, "workspace"), workspace.numel(), _stream())
+    return (draft, choice, logq, S, S0) if scores else (draft, choice, logq)
+
+
+def pair_walk_certified(in_vec: torch.Tensor, out_vec: torch.Tensor, logp: torch.Tensor,
+                        ids: torch.Tensor, E: torch.Tensor, packed: torch.Tensor, anchor_out=None,
+                        sigma: float = SIGMA, logp_weight: float = 0.0,
+                        margin: float = CERT_MARGIN, *, scores: bool = False, out=None,
+                        workspace=None):
+    """Steps 3-4 in one pass, near-tied decisions re-scored in fp64 -> (draft, choice, logq,
+    rescored[, S, S0 when scores=True]); the workspace is score_walk_certified's."""
+    N, B, K, d, *ptrs = _vector_args(in_vec, out_vec, anchor_out, logp, ids)
+    (draft, choice, logq, rescored), S, S0 = _decode_outputs(N, B, K, ids.device, anchor_out,
+                                                             "rescored", scores, out)
+    if workspace is None:
+        workspace = score_walk_certified_workspace(N, B, K, ids.device)
+    lilicorr_pair_walk_certified(
+        *ptrs, _dev(E, "E", (torch.bfloat16, torch.float32)), _dtype_code(E), E.shape[0],
+        _dev(packed, "packed"), N, B, K, d, float(sigma), float(logp_weight), float(margin),
+        _dev(S, "S", (torch.float32,)) if S is not None and B > 1 else None,
+        _dev(S0, "S0", (torch.float32,)), _dev(draft, "draft", (torch.int32,)),
+        _dev(choice, "choice", (torch.int32,)), _dev(logq, "logq", (torch.float32,)),
+        _dev(rescored, "rescored", (torch.int32,)), _dev(workspace, "workspace"),
+        workspace.numel(), _stream())
+    return (draft, choice, logq, rescored, S, S0) if scores else (draft, choice, logq, rescored)
+
+
+def pair_viterbi(in_vec: torch.Tensor, out_vec: torch.Tensor, logp: torch.Tensor,
+                 ids: torch.Tensor, anchor_out=None, sigma: float = SIGMA,
+                 logp_weight: float = 0.0, *, scores: bool = False, out=None, workspace=None):
+    """Steps 3-4 with the exact decode in one pass -> (draft, choice, logq, score[, S, S0 when
+    scores=True]); the workspace is score_viterbi's."""
+    N, B, K, d, *ptrs = _vector_args(in_vec, out_vec, anchor_out, logp, ids)
+    (draft, choice, logq, score), S, S0 = _decode_outputs(N, B, K, ids.device, anchor_out,
+                                                          "score", scores, out)
+    if workspace is None:
+        workspace = score_viterbi_workspace(N, B, K, ids.device)
+    lilicorr_pair_viterbi(*ptrs, N, B, K, d, float(sigma), float(logp_weight),
+                          _dev(S, "S", (torch.float32,)) if S is not None and B > 1 else None,
+                          _dev(S0, "S0", (torch.float32,)), _dev(draft, "draft", (torch.int32,)),
+                          _dev(choice, "choice", (torch.int32,)),
+                          _dev(logq, "logq", (torch.float32,)),
+                          _dev(score, "score", (torch.float32,)), _dev(workspace, "workspace"),
+                          workspace.numel(), _stream())
+    return (draft, choice, logq, score, S, S0) if scores else (draft, choice, logq, score)
 
 
 class BlockGraph:

@@ -34,6 +34,7 @@
 
 #include "certify.hpp"
 #include "common.hpp"
+#include "handover.hpp"
 #include "lilicorr.h"
 #include "projection.hpp"
 #include "viterbi.hpp"
@@ -45,11 +46,6 @@ namespace {
 // every compute unit a workgroup at 64 (a workgroup then holds fewer slot pairs, P = SR / K).
 constexpr int kFillWorkgroups = 256;
 constexpr int kFusedMaxD = 256;              // the fp32 projections of both sides fit in LDS
-constexpr int64_t kMaxTableRows = 16384;     // a request's table is staged in LDS at the end
-constexpr int64_t kMaxExactSlots = 8192;     // exact decode: B bytes of path in LDS
-constexpr int64_t kMaxExactBackPointers = 65536;  // exact decode: B * K bytes of predecessors
-constexpr size_t kExactStageBytes = 64 * 1024;    // exact decode: S[n] staged when it fits
-constexpr size_t kCounterBytes = 256;        // counters are padded to this alignment
 
 struct FusedPlan {
   int sr;            // candidate rows per side per workgroup (64, 32 or 16; K <= sr)
@@ -59,18 +55,14 @@ struct FusedPlan {
   int ws;            // waves per side
   int astride;       // bf16 elements per gathered row in LDS
   int vstride;       // floats per projected row in LDS
-  int64_t rows;      // per request: table rows 1 + (B-1) K (greedy), or floats of score blocks
-                     // and anchor scores (B-1) K K + K (exact)
-  bool stage;        // exact: the last workgroup stages the request's scores in LDS
-  size_t cert_off;   // certified greedy: offset of the re-scoring scratch in the shared region
-  size_t x_bytes;    // shared region: gathered tile, then projections, then (last) the table
+  TailPlan tail;     // the last workgroup's part (table or scores, from the start of LDS)
+  size_t x_bytes;    // shared region: gathered tile, then projections, then (last) the tail
   size_t lds_bytes;  // total dynamic LDS
 };
 
 inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = false, int sr = 64) {
   FusedPlan p;
   p.sr = sr;
-  p.cert_off = 0;
   const VecGeom g = vec_geom(d);
   p.P = sr / K;
   const int64_t pairs = B - 1;
@@ -81,25 +73,9 @@ inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = fal
   p.vstride = d + 4;
   const size_t a_bytes = (size_t)2 * sr * p.astride * 2;
   const size_t v_bytes = (size_t)2 * sr * p.vstride * 4;
-  size_t t_bytes;
-  if (exact) {
-    p.rows = (B - 1) * K * K + K;
-    const int G = K <= 16 ? 16 : (K <= 32 ? 32 : 64);
-    const size_t s_bytes = (size_t)(B - 1) * K * (G + 4) * 4;  // transposed, padded to G + 4
-    p.stage = s_bytes <= kExactStageBytes;
-    t_bytes = 64 * 8 + (p.stage ? s_bytes : 0) + (size_t)(B * K + B);
-  } else {
-    p.rows = 1 + (B - 1) * K;
-    p.stage = false;
-    // table, then per slot: choice, logq (and the re-scoring mark when certified)
-    t_bytes = (size_t)p.rows * 8 + (size_t)B * (cert ? 12 : 8);
-    if (cert) {
-      p.cert_off = (t_bytes + 15) / 16 * 16;
-      t_bytes = p.cert_off + cert_scratch_bytes(d, 2 * p.ws * kWave);
-    }
-  }
+  p.tail = tail_plan(B, K, d, exact, cert, 2 * p.ws * kWave);
   p.x_bytes = a_bytes > v_bytes ? a_bytes : v_bytes;
-  if (t_bytes > p.x_bytes) p.x_bytes = t_bytes;
+  if (p.tail.bytes > p.x_bytes) p.x_bytes = p.tail.bytes;
   p.x_bytes = (p.x_bytes + 15) / 16 * 16;
   p.lds_bytes = p.x_bytes + (size_t)2 * p.ws * sr * 4  // per-wave partial norms
                 + (size_t)2 * sr * 4                   // row squared norms
@@ -107,25 +83,6 @@ inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = fal
                 + (size_t)p.P * K * K * 4                     // this workgroup's scores
                 + 16;                                         // ticket flag
   return p;
-}
-
-inline size_t counter_bytes(int64_t N) {
-  return ((size_t)N * 4 + kCounterBytes - 1) / kCounterBytes * kCounterBytes;
-}
-
-// counters, then the exchange region: score blocks (exact), or table entries and, when
-// certified, one contender mask per table row
-inline size_t fused_workspace_bytes(int64_t N, int64_t B, int K, bool exact, bool cert = false) {
-  if (exact) return counter_bytes(N) + (size_t)N * (size_t)((B - 1) * K * K + K) * 4;
-  return counter_bytes(N) + (size_t)N * (size_t)(1 + (B - 1) * K) * 8 * (cert ? 2 : 1);
-}
-
-// Data one workgroup leaves for the request's last one goes out with device-coherent stores: they
-// leave little dirty in this compute unit's L2 for the release fence to write back (measured:
-// the fused pass 2.6 us faster with the greedy rule, 6.3 us with the exact one).
-template <typename T>
-__device__ __forceinline__ void exchange_store(T* p, T v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int G, bool EXACT, bool CERT, int SR>
@@ -142,7 +99,7 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   uint16_t* A = reinterpret_cast<uint16_t*>(smem);  // [2 SR][astride] gathered rows
   float* Vf = reinterpret_cast<float*>(smem);       // [128][vstride] projections (after A)
-  uint64_t* tbl = reinterpret_cast<uint64_t*>(smem);  // [rows] the request's table (last wg)
+  // (the last workgroup's table or scores start at smem too, after the ticket)
   uint64_t* table = static_cast<uint64_t*>(exchange);   // greedy: [N][rows] table entries
   float* xs = static_cast<float*>(exchange);            // exact: [N][rows] scores
   float* ssw = reinterpret_cast<float*>(smem + plan.x_bytes);  // [2][ws][64]
@@ -288,7 +245,7 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
 
   // ---- 5. transition-table rows, or (exact decode) the score blocks; optional outputs ------
   if (EXACT) {
-    float* xn = xs + n * plan.rows;
+    float* xn = xs + n * plan.tail.rows;
     if (npair > 0)
       for (int i = tid; i < npair * K * K; i += nthreads)
         exchange_store(&xn[(int64_t)t0 * K * K + i], sbuf[i]);
@@ -317,24 +274,11 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
         }
       }
       if (lr < nrows) grow = lr < npair * K ? 1 + (int64_t)t0 * K + lr : 0;
-      int arg;
-      float lq, m;
-      resolve_row<G>(z, live, arg, lq, m);
-      uint32_t lo = (uint32_t)arg;
-      uint64_t cont = 0;
-      if (CERT) {
-        // contenders: every candidate within the margin of the fp32 maximum. Row 0 without an
-        // anchor needs none: its scores are lambda * logp (or 0) on both sides of any comparison.
-        const int gshift = (lane / G) * G;
-        const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
-        cont = (__ballot(live && z >= m - margin) >> gshift) & gmask;
-        if ((lr < npair * K || anchor_wg) && __popcll(cont) > 1) lo |= kCertFlag;
-      }
-      if (j == 0 && grow >= 0) {
-        exchange_store(&table[n * plan.rows + grow],
-                       (uint64_t)lo | ((uint64_t)__float_as_uint(lq) << 32));
-        if (CERT && (lo & kCertFlag)) exchange_store(&cmask[n * plan.rows + grow], cont);
-      }
+      // contenders (certified): row 0 without an anchor needs none, its scores are lambda * logp
+      // (or 0) on both sides of any comparison
+      hand_over_row<G, CERT>(z, live, grow, lr < npair * K || anchor_wg, margin,
+                             table + n * plan.tail.rows,
+                             CERT ? cmask + n * plan.tail.rows : nullptr, j);
     }
   }
   {
@@ -347,105 +291,10 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   }
 
   // ---- 6. ticket; the request's last workgroup walks -----------------------------------------
-  // Everything the last workgroup reads (table rows, score blocks, contender masks) went out with
-  // device-coherent stores: once every wave has waited for its own stores to complete they are
-  // visible to the whole device, and one thread takes the ticket. The certified rule also
-  // releases with a device-wide fence, because its last workgroup overwrites pair scores that
-  // the others wrote with ordinary stores (a write-back of this compute unit's L2 orders them
-  // first). Only the request's last workgroup acquires (a device-wide fence in every thread, or
-  // an acquire in every workgroup, would invalidate cached weights under the other workgroups
-  // still running: measured 2.7x slower).
-  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (tid == 0) {
-    if (CERT) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    const uint32_t done =
-        __hip_atomic_fetch_add(&counters[n], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = done == (uint32_t)(plan.wg - 1);
-    if (*flag) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  }
-  __syncthreads();
-  if (!*flag) return;
-  if (EXACT) {
-    const float* xn = xs + n * plan.rows;
-    const int64_t nS = (B - 1) * (int64_t)K * K;
-    double* line = reinterpret_cast<double*>(smem);   // [64] best path sums of one slot
-    float* T = reinterpret_cast<float*>(line + kWave);  // [B-1][K][G+4] when staged
-    uint8_t* from = reinterpret_cast<uint8_t*>(
-        T + (plan.stage ? (B - 1) * (int64_t)K * viterbi_stride<G>() : 0));
-    const float* S0n = anchor_out ? xn + nS : nullptr;
-    int32_t* choice_n = choice ? choice + n * B : nullptr;
-    float* logq_n = logq ? logq + n * B : nullptr;
-    float* score_n = score ? score + n : nullptr;
-    if (plan.stage) {
-      if (B > 1) stage_transposed<G>(T, xn, B, K, tid, nthreads);
-      __syncthreads();
-      viterbi_block<G, true>(T, S0n, lpn, ids + n * B * K, B, K, lambda, from, from + B * K,
-                             line, draft + n * B, choice_n, logq_n, score_n, tid, nthreads);
-    } else {
-      viterbi_block<G, false>(xn, S0n, lpn, ids + n * B * K, B, K, lambda, from, from + B * K,
-                              line, draft + n * B, choice_n, logq_n, score_n, tid, nthreads);
-    }
-    if (tid == 0) counters[n] = 0u;  // ready for the next call (visible to it at the kernel boundary)
-    return;
-  }
-  for (int64_t i = tid; i < plan.rows; i += nthreads) tbl[i] = table[n * plan.rows + i];
-  int32_t* ch = reinterpret_cast<int32_t*>(tbl + plan.rows);  // [B]
-  float* lq_t = reinterpret_cast<float*>(ch + B);             // [B]
-  int32_t* rs_t = reinterpret_cast<int32_t*>(lq_t + B);       // [B] (certified)
-  __syncthreads();
-  if (CERT) {
-    // every thread follows the table (same entries, so the same branches); a flagged row on the
-    // path is decided again by the whole workgroup
-    const float* w_in = w32;
-    const float* w_out = w32 + (size_t)d * d;
-    const int32_t* idn = ids + n * B * K;
-    int c = 0;
-    for (int64_t t = 0; t < B; ++t) {
-      const int64_t row = t == 0 ? 0 : 1 + (t - 1) * K + c;
-      const uint64_t e = tbl[row];
-      int arg = (int)((uint32_t)e & kArgMask);
-      float lq = __uint_as_float((uint32_t)(e >> 32));
-      int mark = 0;
-      if ((uint32_t)e & kCertFlag) {
-        float dlq;
-        const int best = certify_decision(
-            t == 0 ? anchor_out + n * d : nullptr, t == 0 ? -1 : idn[(t - 1) * K + c],
-            idn + t * K, lpn + t * K, cmask[n * plan.rows + row], arg, E, V, d, w_in, w_out,
-            sigma, lambda,
-            t == 0 ? (S0 ? S0 + n * K : nullptr)
-                   : (S ? S + ((n * (B - 1) + t - 1) * K + c) * (int64_t)K : nullptr),
-            smem + plan.cert_off, tid, nthreads, dlq);
-        mark = best == arg ? 1 : 2;
-        arg = best;
-        lq += dlq;
-      }
-      if (tid == 0) {
-        ch[t] = arg;
-        lq_t[t] = lq;
-        rs_t[t] = mark;
-      }
-      c = arg;
-    }
-    if (tid == 0) counters[n] = 0u;  // ready for the next call (visible to it at the kernel boundary)
-  } else if (tid == 0) {
-    int c = 0;
-    for (int64_t t = 0; t < B; ++t) {
-      const uint64_t e = tbl[t == 0 ? 0 : 1 + (t - 1) * K + c];
-      c = (int)(uint32_t)e;
-      ch[t] = c;
-      lq_t[t] = __uint_as_float((uint32_t)(e >> 32));
-    }
-    counters[n] = 0u;  // ready for the next call (visible to it at the kernel boundary)
-  }
-  __syncthreads();
-  for (int64_t t = tid; t < B; t += nthreads) {
-    const int ct = ch[t];
-    draft[n * B + t] = ids[(n * B + t) * K + ct];
-    if (choice) choice[n * B + t] = ct;
-    if (logq) logq[n * B + t] = lq_t[t];
-    if (CERT && rescored) rescored[n * B + t] = rs_t[t];
-  }
+  if (!take_ticket<CERT>(&counters[n], (uint32_t)plan.wg, flag, tid)) return;
+  TailArgs ta{n, B, V, K, d, sigma, lambda, E, w32, anchor_out, ids, logp, S, S0, draft,
+              choice, logq, score, rescored, &counters[n], exchange, cmask, plan.tail};
+  finish_request<G, EXACT, CERT>(ta, smem, tid, nthreads);
 }
 
 // certified greedy decode only: the re-scoring margin, the fp32 weights (the packed buffer's
@@ -484,12 +333,6 @@ void launch_fused(const FusedPlan& plan, int64_t N, hipStream_t stream, const in
   go(std::integral_constant<int, 64>{});
 }
 
-inline bool fused_shape_ok(int64_t N, int64_t B, int K, bool exact) {
-  if (N < 1 || B < 1 || K < 1 || K > 64) return false;
-  if (exact) return B <= kMaxExactSlots && B * K <= kMaxExactBackPointers;
-  return B <= kMaxTableRows && 1 + (B - 1) * (int64_t)K <= kMaxTableRows;
-}
-
 template <bool EXACT, bool CERT, bool CHECK_ONLY = false>
 lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const void* E,
                                  lilicorr_dtype e_dtype, int64_t V, int d, const void* packed_w,
@@ -505,14 +348,14 @@ lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const vo
   if (CERT && !(isfinite(margin) && margin >= 0.f)) return LILICORR_ERR_INVALID_ARG;
   if (e_dtype != LILICORR_BF16) return LILICORR_ERR_UNSUPPORTED;
   if (d % 16 != 0 || d > kFusedMaxD || V >= ((int64_t)1 << 31)) return LILICORR_ERR_UNSUPPORTED;
-  if (!fused_shape_ok(N, B, K, EXACT)) return LILICORR_ERR_UNSUPPORTED;
+  if (!decode_shape_ok(N, B, K, EXACT)) return LILICORR_ERR_UNSUPPORTED;
   if (!aligned16(ids) || !aligned16(logp) || !aligned16(E) || !aligned16(packed_w) ||
       !aligned16(draft) || !aligned16(workspace) || (anchor_out && !aligned16(anchor_out)) ||
       (S && !aligned16(S)) || (S0 && !aligned16(S0)) || (choice && !aligned16(choice)) ||
       (logq && !aligned16(logq)) || (score && !aligned16(score)) ||
       (rescored && !aligned16(rescored)))
     return LILICORR_ERR_ALIGNMENT;
-  if (workspace_bytes < fused_workspace_bytes(N, B, K, EXACT, CERT)) return LILICORR_ERR_WORKSPACE;
+  if (workspace_bytes < decode_workspace_bytes(N, B, K, EXACT, CERT)) return LILICORR_ERR_WORKSPACE;
   // the largest rows-per-side that still gives the chip kFillWorkgroups workgroups (or 16 rows,
   // the smallest block, when even that does not); never below K
   int sr = 64;
@@ -533,7 +376,7 @@ lilicorr_status score_and_decode(const int32_t* ids, const float* logp, const vo
   CertArgs ca{margin, nullptr, nullptr, rescored};
   if (CERT) {
     ca.w32 = reinterpret_cast<const float*>(frags + frag_bytes(d));
-    ca.cmask = static_cast<uint64_t*>(exchange) + N * plan.rows;
+    ca.cmask = static_cast<uint64_t*>(exchange) + N * plan.tail.rows;
   }
   if (K <= 16)
     launch_fused<16, EXACT, CERT>(plan, N, stream, ids, logp, e16, V, d, frags, g.nbp, g.dkp,
@@ -606,9 +449,9 @@ extern "C" lilicorr_status lilicorr_score_walk_noalloc(
   // the limits and argument checks of lilicorr_score_walk come first (its own status codes);
   // then the scratch size
   if (!ids || !logp || !E || !packed_w || !draft) return LILICORR_ERR_INVALID_ARG;
-  if (!fused_shape_ok(N, B, K, false)) return N < 1 || B < 1 || K < 1 ? LILICORR_ERR_INVALID_ARG
+  if (!decode_shape_ok(N, B, K, false)) return N < 1 || B < 1 || K < 1 ? LILICORR_ERR_INVALID_ARG
                                                                         : LILICORR_ERR_UNSUPPORTED;
-  const size_t need = fused_workspace_bytes(N, B, K, false);
+  const size_t need = decode_workspace_bytes(N, B, K, false);
   if (need > kNoAllocScratchBytes) return LILICORR_ERR_WORKSPACE;
   lilicorr_status err = LILICORR_OK;
   unsigned char* ws = scratch_address(&err);
@@ -628,7 +471,7 @@ extern "C" lilicorr_status lilicorr_score_walk_noalloc(
 }
 
 extern "C" size_t lilicorr_score_walk_workspace_bytes(int64_t N, int64_t B, int K) {
-  return fused_shape_ok(N, B, K, false) ? fused_workspace_bytes(N, B, K, false) : 0;
+  return decode_shape_ok(N, B, K, false) ? decode_workspace_bytes(N, B, K, false) : 0;
 }
 
 extern "C" lilicorr_status lilicorr_score_walk(
@@ -642,7 +485,7 @@ extern "C" lilicorr_status lilicorr_score_walk(
 }
 
 extern "C" size_t lilicorr_score_walk_certified_workspace_bytes(int64_t N, int64_t B, int K) {
-  return fused_shape_ok(N, B, K, false) ? fused_workspace_bytes(N, B, K, false, true) : 0;
+  return decode_shape_ok(N, B, K, false) ? decode_workspace_bytes(N, B, K, false, true) : 0;
 }
 
 extern "C" lilicorr_status lilicorr_score_walk_certified(
@@ -656,7 +499,7 @@ extern "C" lilicorr_status lilicorr_score_walk_certified(
 }
 
 extern "C" size_t lilicorr_score_viterbi_workspace_bytes(int64_t N, int64_t B, int K) {
-  return fused_shape_ok(N, B, K, true) ? fused_workspace_bytes(N, B, K, true) : 0;
+  return decode_shape_ok(N, B, K, true) ? decode_workspace_bytes(N, B, K, true) : 0;
 }
 
 extern "C" lilicorr_status lilicorr_score_viterbi(

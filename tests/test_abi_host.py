@@ -32,7 +32,8 @@ def test_header_declares_the_path(L):
               "lilicorr_score_walk_certified", "lilicorr_score_walk_certified_workspace_bytes",
               "lilicorr_block_graph_create", "lilicorr_block_graph_launch",
               "lilicorr_block_graph_destroy", "lilicorr_status_string",
-              "lilicorr_topk_wait_status", "lilicorr_set_wait_limit"]:
+              "lilicorr_topk_wait_status", "lilicorr_set_wait_limit", "lilicorr_pair_walk",
+              "lilicorr_pair_walk_certified", "lilicorr_pair_viterbi"]:
         assert n in names
 
 
@@ -292,6 +293,76 @@ def test_score_viterbi_sizes_and_argument_errors(L):
     assert call(5, 512) == -2         # d above the fused pass
     assert call(18, A + 4) == -3      # score alignment
     assert call(20, ws - 1) == -4
+
+
+def test_pair_walk_argument_errors(L):
+    """The one-pass decode over precomputed vectors: any width the vector call supports (d <= 1024;
+    certified d <= 512 with bf16 rows), the fused calls' workspaces."""
+    lib = L.load_library()
+    ws = L.lilicorr_score_walk_workspace_bytes(2, 3, 4)
+    names = ["in", "out", "anchor", "logp", "ids", "N", "B", "K", "d", "sigma", "lw", "S", "S0",
+             "draft", "choice", "logq", "ws", "ws_bytes", "stream"]
+    ok = [A, A, None, A, A, 2, 3, 4, 512, 8.0, 0.0, None, None, A, None, None, A, ws, None]
+
+    def call(**kw):
+        args = list(ok)
+        for k, v in kw.items():
+            args[names.index(k)] = v
+        return lib.lilicorr_pair_walk(*args)
+    assert call(**{"in": None}) == -1
+    assert call(out=None) == -1
+    assert call(ids=None) == -1
+    assert call(draft=None) == -1
+    assert call(ws=None) == -1
+    assert call(N=0) == -1
+    assert call(sigma=float("nan")) == -1
+    assert call(d=40) == -2
+    assert call(d=1040) == -2
+    assert call(K=65) == -2
+    assert call(B=20000, K=1) == -2
+    assert call(N=65536) == -2
+    assert call(out=A + 4) == -3
+    assert call(logq=A + 8) == -3
+    assert call(ws_bytes=ws - 1) == -4
+
+    wsc = L.lilicorr_score_walk_certified_workspace_bytes(2, 3, 4)
+    cnames = ["in", "out", "anchor", "logp", "ids", "E", "e_dtype", "V", "packed", "N", "B", "K",
+              "d", "sigma", "lw", "margin", "S", "S0", "draft", "choice", "logq", "rescored", "ws",
+              "ws_bytes", "stream"]
+    cok = [A, A, None, A, A, A, 1, 1000, A, 2, 3, 4, 512, 8.0, 0.0, 2.0 ** -14, None, None, A,
+           None, None, None, A, wsc, None]
+
+    def ccall(**kw):
+        args = list(cok)
+        for k, v in kw.items():
+            args[cnames.index(k)] = v
+        return lib.lilicorr_pair_walk_certified(*args)
+    assert ccall(E=None) == -1
+    assert ccall(packed=None) == -1
+    assert ccall(V=0) == -1
+    assert ccall(e_dtype=7) == -1
+    assert ccall(margin=-1.0) == -1
+    assert ccall(e_dtype=0) == -2       # the re-scoring reads bf16 rows
+    assert ccall(d=528) == -2           # one vector per 512 threads at most
+    assert ccall(packed=A + 4) == -3
+    assert ccall(rescored=A + 4) == -3
+    assert ccall(ws_bytes=ws) == -4     # the plain pass's workspace lacks the contender masks
+
+    wse = L.lilicorr_score_viterbi_workspace_bytes(2, 3, 4)
+    enames = ["in", "out", "anchor", "logp", "ids", "N", "B", "K", "d", "sigma", "lw", "S", "S0",
+              "draft", "choice", "logq", "score", "ws", "ws_bytes", "stream"]
+    eok = [A, A, None, A, A, 2, 3, 4, 1024, 8.0, 0.0, None, None, A, None, None, None, A, wse, None]
+
+    def ecall(**kw):
+        args = list(eok)
+        for k, v in kw.items():
+            args[enames.index(k)] = v
+        return lib.lilicorr_pair_viterbi(*args)
+    assert ecall(logp=None) == -1
+    assert ecall(B=8193, K=1) == -2
+    assert ecall(B=2000, K=64) == -2
+    assert ecall(score=A + 4) == -3
+    assert ecall(ws_bytes=wse - 1) == -4
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

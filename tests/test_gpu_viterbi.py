@@ -106,7 +106,7 @@ def test_viterbi_planted_near_ties(lib, seed):
         assert tuple(g[1][n]) == _exact_best(S, S0, n, B, K), (seed, n)
 
 
-@pytest.mark.parametrize("cfg_index", [1, 2, 3])
+@pytest.mark.parametrize("cfg_index", [1, 2, 3, 4])
 def test_viterbi_on_oracle_chain_scores(lib, oracle_chain, cfg_index):
     """The exact decode over the oracle chain's own pair scores, every request: bit-exact paths
     against the oracle chain's exact decode."""

@@ -5,7 +5,9 @@ Walk: on identical S / S0 / logp / ids the draft and choice are bit-exact and lo
 greedy_walk on one stream and the oracle runs its own chain on the same seeded inputs; drafts
 must be bit-exact for every request of every config (the oracle chain of configs 2-4 runs one
 request per task on a thread pool). A mismatch reports the oracle's top-2 score gap at the
-decision where the two walks part.
+decision where the two walks part. The same GPU chain then takes the exact max-path decode
+(lilicorr_viterbi_walk on the GPU's pair scores) and its paths must equal the oracle chain's exact
+decode on the oracle's own scores, again for every request.
 """
 import os
 
@@ -16,7 +18,7 @@ import yaml
 
 import oracle
 import workloads
-from parity import assert_close, assert_equal, greedy_gap, to_np
+from parity import assert_close, assert_equal, greedy_gap, path_gap, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -86,10 +88,12 @@ def test_chain_drafts_bit_exact(lib, cfg_inputs, oracle_chain, cfg_index):
     E = inp["E"].cuda()
     packed = lib.pack_weights(inp["W_in"].cuda(), inp["W_out"].cuda())
     out = lib.draft_block(logits, cfg.K, E, packed)
+    vd, vc, vq, vs = lib.viterbi_walk(out["S"], out["S0"], out["logp"], out["ids"])
     torch.cuda.synchronize()
     g = {k: (to_np(v) if v is not None else None) for k, v in out.items()
          if k not in ("in_vec", "out_vec")}
-    del logits, out
+    g.update(vdraft=to_np(vd), vchoice=to_np(vc), vlogq=to_np(vq), vscore=to_np(vs))
+    del logits, out, vd, vc, vq, vs
     r = oracle_chain(cfg_index)
     what = f"cfg{cfg_index} ({cfg.N} requests)"
     assert_equal(g["ids"], r["ids"], f"{what} ids")
@@ -103,6 +107,15 @@ def test_chain_drafts_bit_exact(lib, cfg_inputs, oracle_chain, cfg_index):
                              f"oracle top-2 gap {greedy_gap(r['S'], None, r['choice'], n, t):.3e}")
     assert_equal(g["draft"], r["draft"], f"{what} draft")
     assert_close(g["logq"], r["logq"], f"{what} logq")
+    # exact decode: the GPU chain's paths against the oracle chain's (each on its own scores)
+    bad = np.argwhere((g["vchoice"] != r["vchoice"]).any(axis=1))
+    if bad.size:
+        n = int(bad[0, 0])
+        raise AssertionError(f"{what}: exact-decode paths differ in {bad.size} requests; request "
+                             f"{n}: oracle best-to-second path gap {path_gap(r['S'], None, n):.3e}")
+    assert_equal(g["vdraft"], r["vdraft"], f"{what} exact draft")
+    assert_close(g["vlogq"], r["vlogq"], f"{what} exact logq")
+    assert_close(g["vscore"], r["vscore"], f"{what} exact score")
 
 
 def test_chain_with_anchor(lib, cfg_inputs):
