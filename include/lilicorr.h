@@ -351,7 +351,10 @@ lilicorr_status lilicorr_pair_viterbi(const float *in_vec, const float *out_vec,
  * One draft block as one HIP graph (implementation appendix, serving: candidate extraction,
  * matching and selection replayed as one graph per block). lilicorr_block_graph_create records
  * lilicorr_topk followed by one fused pass (greedy, certified greedy or exact decode) with the
- * arguments below, on a stream of its own, without running anything; every replay then runs the
+ * arguments below, on a stream of its own, without running anything. Where the fused pass does
+ * not apply (fp32 E, or d above 256) it records lilicorr_candidate_vectors into in_vec / out_vec
+ * followed by the one-pass decode over them (lilicorr_pair_walk, lilicorr_pair_walk_certified or
+ * lilicorr_pair_viterbi, with the same fused_workspace) instead; every replay then runs the
  * block on whatever the buffers hold at that time. The graph keeps the pointers: the buffers
  * must stay allocated, at the same addresses, until the graph is destroyed, and replays that
  * share buffers must not overlap in time. Unlike the calls above, create allocates the graph's
@@ -393,6 +396,8 @@ typedef struct {
     int32_t *rescored;  /* certified only, optional */
     void *fused_workspace;
     size_t fused_workspace_bytes;
+    /* [N][B][K][d] fp32 each: required where the fused pass does not apply, else unused */
+    float *in_vec, *out_vec;
 } lilicorr_block_args;
 
 typedef struct lilicorr_graph lilicorr_graph;

@@ -77,6 +77,7 @@ class BlockArgs(ctypes.Structure):
         ("draft", ctypes.c_void_p), ("choice", ctypes.c_void_p), ("logq", ctypes.c_void_p),
         ("score", ctypes.c_void_p), ("rescored", ctypes.c_void_p),
         ("fused_workspace", ctypes.c_void_p), ("fused_workspace_bytes", ctypes.c_size_t),
+        ("in_vec", ctypes.c_void_p), ("out_vec", ctypes.c_void_p),
     ]
 
 
@@ -647,8 +648,10 @@ class BlockGraph:
     """One draft block (top-K, then one fused pass) recorded as a HIP graph over fixed buffers.
 
     The outputs (ids, logp, draft, choice, logq, and score / rescored / S / S0 where they apply)
-    are allocated here; launch() replays the block on the current stream over whatever `logits`
-    holds then. The object keeps every buffer the graph points at alive until close().
+    are allocated here, and so are the in/out vector buffers where the fused pass does not apply
+    (fp32 E or d above 256: the graph then holds the candidate vectors and the one-pass decode
+    over them); launch() replays the block on the current stream over whatever `logits` holds
+    then. The object keeps every buffer the graph points at alive until close().
     """
 
     def __init__(self, logits: torch.Tensor, K: int, E: torch.Tensor, packed: torch.Tensor,
@@ -678,6 +681,10 @@ class BlockGraph:
         ws_fn = {"greedy": score_walk_workspace, "certified": score_walk_certified_workspace,
                  "exact": score_viterbi_workspace}[decode]
         self.fused_workspace = ws_fn(N, B, K, dev)
+        self.in_vec = self.out_vec = None
+        if E.dtype != torch.bfloat16 or d > 256:
+            self.in_vec = torch.empty(N, B, K, d, dtype=torch.float32, device=dev)
+            self.out_vec = torch.empty_like(self.in_vec)
         a = BlockArgs()
         a.logits = _dev(logits, "logits", (torch.bfloat16, torch.float32))
         a.logits_dtype = _dtype_code(logits)
@@ -700,6 +707,8 @@ class BlockGraph:
         a.rescored = self.rescored.data_ptr() if self.rescored is not None else None
         a.fused_workspace = self.fused_workspace.data_ptr()
         a.fused_workspace_bytes = self.fused_workspace.numel()
+        if self.in_vec is not None:
+            a.in_vec, a.out_vec = self.in_vec.data_ptr(), self.out_vec.data_ptr()
         self.args = a
         self._graph = lilicorr_block_graph_create(a)
 
