@@ -261,6 +261,30 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10, batches=10):
     if L.topk_wait_status(ws) != 0:
         raise RuntimeError("a bounded wait of the logits pass gave up: outputs invalid")
     read = stream_read_rate(torch, lgs, iters=max(10, min(100, copies * 4)))
+    rules = None
+    if not fused:
+        # steps 3-4 over the vectors of the last step: each decode rule in one pass, and the two
+        # separate calls it replaces
+        S = torch.empty(N, max(B - 1, 1), K, K, dtype=torch.float32, device="cuda")
+        score = torch.empty(N, dtype=torch.float32, device="cuda")
+        resc = torch.empty(N, B, dtype=torch.int32, device="cuda")
+        ws_x = L.score_viterbi_workspace(N, B, K)
+        ws_c = L.score_walk_certified_workspace(N, B, K)
+        rules = {
+            "pair_walk_us": median_launch_us(torch, lambda: L.pair_walk(
+                in_vec, out_vec, logp, ids, out=(draft, choice, logq), workspace=ws_fused)),
+            "pair_viterbi_us": median_launch_us(torch, lambda: L.pair_viterbi(
+                in_vec, out_vec, logp, ids, out=(draft, choice, logq, score), workspace=ws_x)),
+            "separate_pair_scores_greedy_walk_us": median_launch_us(torch, lambda: (
+                L.pair_scores(in_vec, out_vec, out=(S, None)),
+                L.greedy_walk(S, None, logp, ids, out=(draft, choice, logq)))),
+            "note": "median call durations (HIP events, host launch included)",
+        }
+        if E.dtype == torch.bfloat16:
+            rules["pair_walk_certified_us"] = median_launch_us(torch, lambda: L.pair_walk_certified(
+                in_vec, out_vec, logp, ids, E, packed, out=(draft, choice, logq, resc),
+                workspace=ws_c))
+            rules["certified_rescored"] = int((resc > 0).sum())
     return {"workload": f"{c.name}: N={N}, B={B}, K={K}, V={V}, d={c.d}, "
                         f"{'bf16' if lg.element_size() == 2 else 'fp32'} logits",
             "path": "lilicorr_topk -> " + ("lilicorr_score_walk" if fused else
@@ -270,7 +294,8 @@ def per_config_rates(L, torch, c, inp, iters=100, warmup=10, batches=10):
             "logits_GB_s": nbytes / t_topk / 1e9, "logits_us": t_topk * 1e6,
             "logits_batches": spread(topks),
             "logits_frac_of_8TBs": nbytes / t_topk / 1e9 / PEAK_HBM_GBS,
-            "stream_read_GB_s": read, "logits_frac_of_stream_read": nbytes / t_topk / 1e9 / read}
+            "stream_read_GB_s": read, "logits_frac_of_stream_read": nbytes / t_topk / 1e9 / read,
+            "decode_rules": rules}
 
 
 PEAK_BF16_TFLOPS = 2500.0

@@ -73,8 +73,11 @@ inline FusedPlan fused_plan(int64_t B, int K, int d, bool exact, bool cert = fal
   p.vstride = d + 4;
   const size_t a_bytes = (size_t)2 * sr * p.astride * 2;
   const size_t v_bytes = (size_t)2 * sr * p.vstride * 4;
-  p.tail = tail_plan(B, K, d, exact, cert, 2 * p.ws * kWave);
+  // the exact decode stages its scores when they fit in the region the tile and projections
+  // already take (at least 64 KB)
   p.x_bytes = a_bytes > v_bytes ? a_bytes : v_bytes;
+  p.tail = tail_plan(B, K, d, exact, cert, 2 * p.ws * kWave,
+                     p.x_bytes > 64 * 1024 ? p.x_bytes : 64 * 1024);
   if (p.tail.bytes > p.x_bytes) p.x_bytes = p.tail.bytes;
   p.x_bytes = (p.x_bytes + 15) / 16 * 16;
   p.lds_bytes = p.x_bytes + (size_t)2 * p.ws * sr * 4  // per-wave partial norms
@@ -291,7 +294,7 @@ __global__ __launch_bounds__(512) void score_walk_kernel(
   }
 
   // ---- 6. ticket; the request's last workgroup walks -----------------------------------------
-  if (!take_ticket<CERT>(&counters[n], (uint32_t)plan.wg, flag, tid)) return;
+  if (!take_ticket(&counters[n], (uint32_t)plan.wg, flag, tid, CERT && (S || S0))) return;
   TailArgs ta{n, B, V, K, d, sigma, lambda, E, w32, anchor_out, ids, logp, S, S0, draft,
               choice, logq, score, rescored, &counters[n], exchange, cmask, plan.tail};
   finish_request<G, EXACT, CERT>(ta, smem, tid, nthreads);

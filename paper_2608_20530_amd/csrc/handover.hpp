@@ -26,7 +26,6 @@ namespace lilicorr {
 constexpr int64_t kMaxTableRows = 16384;          // greedy: the request's table is staged in LDS
 constexpr int64_t kMaxExactSlots = 8192;          // exact decode: B bytes of path in LDS
 constexpr int64_t kMaxExactBackPointers = 65536;  // exact decode: B * K bytes of predecessors
-constexpr size_t kExactStageBytes = 64 * 1024;    // exact decode: S[n] staged when it fits
 constexpr size_t kCounterBytes = 256;             // counters are padded to this alignment
 
 inline bool decode_shape_ok(int64_t N, int64_t B, int K, bool exact) {
@@ -52,15 +51,19 @@ struct TailPlan {
   size_t bytes;     // LDS bytes the last workgroup needs
 };
 
-inline TailPlan tail_plan(int64_t B, int K, int d, bool exact, bool cert, int nthreads) {
+// stage_limit: LDS bytes the exact decode may use with its scores staged (it reads them from the
+// workspace otherwise)
+inline TailPlan tail_plan(int64_t B, int K, int d, bool exact, bool cert, int nthreads,
+                          size_t stage_limit) {
   TailPlan p;
   p.cert_off = 0;
   if (exact) {
     p.rows = (B - 1) * K * K + K;
     const int G = K <= 16 ? 16 : (K <= 32 ? 32 : 64);
     const size_t s_bytes = (size_t)(B - 1) * K * (G + 4) * 4;  // transposed, padded to G + 4
-    p.stage = s_bytes <= kExactStageBytes;
-    p.bytes = 64 * 8 + (p.stage ? s_bytes : 0) + (size_t)(B * K + B);
+    const size_t other = 64 * 8 + (size_t)(B * K + B);
+    p.stage = other + s_bytes <= stage_limit;
+    p.bytes = other + (p.stage ? s_bytes : 0);
   } else {
     p.rows = 1 + (B - 1) * K;
     p.stage = false;
@@ -108,16 +111,17 @@ __device__ __forceinline__ void hand_over_row(float z, bool live, int64_t grow, 
 
 // Every thread of the workgroup calls this after its exchange stores. Each wave waits for its own
 // stores to complete (device-coherent stores are then visible to the whole device); one thread
-// takes the ticket. The certified rule also releases with a device-wide fence, because its last
-// workgroup overwrites pair scores the others wrote with ordinary stores. Only the request's last
-// workgroup acquires (a device-wide fence in every workgroup would invalidate cached data under
-// the workgroups still running). Returns true in every thread of the request's last workgroup.
-template <bool CERT>
-__device__ __forceinline__ bool take_ticket(uint32_t* counter, uint32_t nwg, int* flag, int tid) {
+// takes the ticket. With `release` (the certified rule when pair scores are written out) it also
+// releases with a device-wide fence, because the last workgroup may overwrite pair scores the
+// others wrote with ordinary stores. Only the request's last workgroup acquires (a device-wide
+// fence in every workgroup would invalidate cached data under the workgroups still running).
+// Returns true in every thread of the request's last workgroup.
+__device__ __forceinline__ bool take_ticket(uint32_t* counter, uint32_t nwg, int* flag, int tid,
+                                            bool release) {
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0) {
-    if (CERT) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (release) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     const uint32_t done =
         __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *flag = done == nwg - 1;

@@ -189,7 +189,8 @@ constexpr int kPairWaves = 8;  // matrices (waves) per workgroup of the one-pass
 // matrix (the request's last workgroup may have fewer than eight) only take part in the
 // workgroup's barriers.
 template <int NB, int S4, int G, bool EXACT, bool CERT>
-__global__ __launch_bounds__(kPairWaves * kWave) void pair_walk_kernel(
+__global__ __launch_bounds__(kPairWaves * kWave)
+__attribute__((amdgpu_waves_per_eu(NB <= 2 ? 4 : 2))) void pair_walk_kernel(
     const float* __restrict__ in_vec, const float* __restrict__ out_vec,
     const float* __restrict__ anchor_out, const float* __restrict__ logp,
     const int32_t* __restrict__ ids, const uint16_t* __restrict__ E, int64_t V, int64_t B, int K,
@@ -258,7 +259,7 @@ __global__ __launch_bounds__(kPairWaves * kWave) void pair_walk_kernel(
       hand_over_row<G, CERT>(z, live, grow, lr < prow || anchor, margin, table_n, cmask_n, j);
     }
   }
-  if (!take_ticket<CERT>(&counters[n], gridDim.x, flag, tid)) return;
+  if (!take_ticket(&counters[n], gridDim.x, flag, tid, CERT && (S || S0))) return;
   TailArgs ta{n, B, V, K, d, sigma, lambda, E, w32, anchor_out, ids, logp, S, S0, draft,
               choice, logq, score, rescored, &counters[n], exchange, cmask, tail};
   finish_request<G, EXACT, CERT>(ta, smem, tid, kPairWaves * kWave);
@@ -313,7 +314,7 @@ lilicorr_status pairs_and_decode(const float* in_vec, const float* out_vec,
       (rescored && !aligned16(rescored)) || (CERT && (!aligned16(E) || !aligned16(packed_w))))
     return LILICORR_ERR_ALIGNMENT;
   if (workspace_bytes < decode_workspace_bytes(N, B, K, EXACT, CERT)) return LILICORR_ERR_WORKSPACE;
-  const TailPlan tail = tail_plan(B, K, d, EXACT, CERT, kPairWaves * kWave);
+  const TailPlan tail = tail_plan(B, K, d, EXACT, CERT, kPairWaves * kWave, 160 * 1024 - 16);
   const size_t sw_bytes = EXACT ? 0 : (size_t)kPairWaves * K * K * 4;
   const size_t flag_off = ((sw_bytes > tail.bytes ? sw_bytes : tail.bytes) + 15) / 16 * 16;
   const size_t lds = flag_off + 16;

@@ -1,7 +1,8 @@
 // The exact max-path decode of the decode-rule appendix: the path maximising the sum of its
 // matching terms, Eq. (pathscore), by dynamic programming in O(B K^2), and the local
 // log-likelihoods of Eq. (localar) along that path. One workgroup per request; its score
-// matrices are staged into LDS when they fit, and the sweep itself is viterbi_block.
+// matrices are staged into LDS when they fit (up to the 160 KB of a compute unit), and the sweep
+// itself is viterbi_block.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -16,7 +17,7 @@ namespace {
 constexpr int kViterbiThreads = 256;
 constexpr int64_t kMaxSlots = 8192;
 constexpr int64_t kMaxBackPointers = 65536;  // B * K bytes of predecessors in LDS
-constexpr size_t kStageBytes = 64 * 1024;    // S[n] is staged (transposed) when it fits
+constexpr size_t kMaxLds = 160 * 1024;       // S[n] is staged (transposed) when it fits
 
 template <int G>
 __global__ __launch_bounds__(kViterbiThreads) void viterbi_walk_kernel(
@@ -55,7 +56,7 @@ void launch_viterbi(int64_t N, int64_t B, int K, hipStream_t stream, const float
                     int32_t* draft, int32_t* choice, float* logq, float* score) {
   const size_t head = ((size_t)(B * K + B) + 15) / 16 * 16 + kWave * sizeof(double);
   const size_t t_bytes = (size_t)(B - 1) * K * viterbi_stride<G>() * sizeof(float);
-  const bool stage = B > 1 && t_bytes <= kStageBytes;
+  const bool stage = B > 1 && head + t_bytes <= kMaxLds;
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(viterbi_walk_kernel<G>),
       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);

@@ -115,13 +115,27 @@ __device__ __forceinline__ void viterbi_block(const float* Sv, const float* S0n,
           }
         }
       } else {
+        // lane k's column of S[t-1], loaded 16 predecessors at a time ahead of their scan (one
+        // memory latency per 16 predecessors rather than one per predecessor)
         const float* St = Sv + (t - 1) * (int64_t)K * K;
-        bv = line[0] + (double)(live ? St[k] : 0.f);
-        for (int p = 1; p < K; ++p) {
-          const double v = line[p] + (double)(live ? St[p * K + k] : 0.f);
-          if (v > bv) {
-            bv = v;
-            bp = p;
+        constexpr int kBatch = 16;
+        bv = -__builtin_inf();
+#pragma unroll
+        for (int p0 = 0; p0 < G; p0 += kBatch) {
+          float c[kBatch];
+#pragma unroll
+          for (int q = 0; q < kBatch; ++q)
+            c[q] = live && p0 + q < K ? St[(p0 + q) * K + k] : 0.f;
+#pragma unroll
+          for (int q = 0; q < kBatch; ++q) {
+            const int p = p0 + q;
+            if (p < K) {
+              const double v = line[p] + (double)c[q];
+              if (p == 0 || v > bv) {
+                bv = v;
+                bp = p;
+              }
+            }
           }
         }
       }
