@@ -281,9 +281,12 @@ __global__ __launch_bounds__(512) void cand_vectors_stream_kernel(
 //    term displacements are scalar), in pieces of two column blocks with three pieces in flight.
 //  * Nothing spills: a value reloaded from scratch in the output phase would make each 16-row
 //    block of stores wait for the previous block's to complete.
-//  * The unit vectors go out through a small per-wave LDS staging area, so each non-temporal
-//    store instruction covers whole 128-byte lines (two rows x 512 bytes): 16-byte pieces of
-//    16 rows per instruction wrote 1.5x the bytes to HBM, and ordinary stores left the next
+//  * The unit vectors go out through LDS half 1, free between the last k-block and the next
+//    tile's first copies into it: each wave stages 32 rows x its 128 columns at a time (four
+//    rounds per tile) and reads them back so that each non-temporal store instruction covers
+//    whole 128-byte lines (two rows x 512 bytes): 16-byte pieces of 16 rows per instruction
+//    wrote 1.5x the bytes to HBM, 8-row rounds through a separate staging area took 1.2 us
+//    more per tile, and ordinary stores left the next
 //    kernel's reads behind the L2's write-backs.
 //  * Products run with the weight fragment as the first operand, so each lane ends up holding
 //    four consecutive columns of one row.
@@ -295,7 +298,10 @@ constexpr int kWideDkp = 16;    // 32-deep k-blocks
 constexpr int kHalfChunks = 32; // 16-byte chunks per half row (256 bf16)
 constexpr int kHalfStride = kHalfChunks * 16 + 16;  // bytes per half row in LDS (padded)
 constexpr size_t kWideHalfBytes = (size_t)kWideRows * kHalfStride;
+constexpr int kStageRows = 32;                  // output rows per wave per staging round
 constexpr int kStageStride = kWideNb * 16 + 4;  // floats per staged output row (padded)
+static_assert((size_t)kWideWaves * kStageRows * kStageStride * sizeof(float) <= kWideHalfBytes,
+              "the output staging fits in LDS half 1");
 
 // B fragments of one piece through a buffer descriptor: one lane offset, the k-block and term
 // displacements in the scalar offset, the column-block steps in the instruction offset
@@ -338,7 +344,6 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
   unsigned char* A = smem;                                                // [2][ROWS][32][16 B]
   float* ssbuf = reinterpret_cast<float*>(smem + 2 * kWideHalfBytes);    // [NW][ROWS]
   int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + NW * ROWS);          // [2][ROWS]
-  float* stage_all = reinterpret_cast<float*>(rid + 2 * ROWS);           // [NW][8][kStageStride]
   const size_t slice = (size_t)nbp * 1024;
   const int64_t step = gridDim.x;
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -499,38 +504,39 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     int le = lane;
     __asm__ volatile("" : "+v"(le));
     const int er = le & 15, eg = le >> 4;
-    // each 16-row block goes out in two rounds of 8 rows through this wave's staging rows, read
-    // back so that each half wave writes 128 contiguous columns (512 bytes, whole lines) of one
-    // row with non-temporal stores
-    float* stage = stage_all + wave * 8 * kStageStride;
+    // the output leaves through LDS half 1 (free until the next tile's copies into it begin):
+    // each wave stages kStageRows rows x its 128 columns at a time, read back so that each half
+    // wave writes 512 contiguous bytes (whole lines) of one row with non-temporal stores
+    float* stage = reinterpret_cast<float*>(A + kWideHalfBytes) + wave * kStageRows * kStageStride;
     const int col_w = wave * kWideNb * 16;
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      const int rl = mb * 16 + er;
-      float tot = 0.f;
+    for (int rnd = 0; rnd < ROWS / kStageRows; ++rnd) {
 #pragma unroll
-      for (int w = 0; w < NW; ++w) tot += ssbuf[w * ROWS + rl];
-      const float inv = tot > 0.f ? 1.0f / sqrtf(tot) : 0.f;
+      for (int m2 = 0; m2 < kStageRows / 16; ++m2) {
+        const int mb = rnd * (kStageRows / 16) + m2;
+        const int rl = mb * 16 + er;
+        float tot = 0.f;
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        if ((er >> 3) == half) {
+        for (int w = 0; w < NW; ++w) tot += ssbuf[w * ROWS + rl];
+        const float inv = tot > 0.f ? 1.0f / sqrtf(tot) : 0.f;
 #pragma unroll
-          for (int nb = 0; nb < kWideNb; ++nb)
-            *reinterpret_cast<f32x4*>(stage + (er & 7) * kStageStride + nb * 16 + eg * 4) =
-                acc[mb][nb] * inv;
-        }
+        for (int nb = 0; nb < kWideNb; ++nb)
+          *reinterpret_cast<f32x4*>(stage + (m2 * 16 + er) * kStageStride + nb * 16 + eg * 4) =
+              acc[mb][nb] * inv;
+      }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int sr = 2 * q + (le >> 5);
-          const int64_t r = row0 + mb * 16 + half * 8 + sr;
-          const int col = col_w + (le & 31) * 4;
-          const f32x4 v =
-              *reinterpret_cast<const f32x4*>(stage + sr * kStageStride + (le & 31) * 4);
-          if (r < M && col < d)
-            __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(&out[r * d + col]));
-        }
+      for (int q = 0; q < kStageRows / 2; ++q) {
+        const int sr = 2 * q + (le >> 5);
+        const int64_t r = row0 + rnd * kStageRows + sr;
+        const int col = col_w + (le & 31) * 4;
+        const f32x4 v =
+            *reinterpret_cast<const f32x4*>(stage + sr * kStageStride + (le & 31) * 4);
+        if (r < M && col < d)
+          __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(&out[r * d + col]));
       }
     }
+    // every wave has read its staged rows back before the next tile's copies go into half 1
+    __syncthreads();
   }
 }
 
@@ -681,8 +687,7 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
       const int64_t wt = 2 * ((M + kWideRows - 1) / kWideRows);
       const int grid = (int)(wt < ncu ? wt : ncu);
       const size_t lds = 2 * kWideHalfBytes + (size_t)kWideWaves * kWideRows * sizeof(float) +
-                         (size_t)2 * kWideRows * sizeof(int32_t) +
-                         (size_t)kWideWaves * 8 * kStageStride * sizeof(float);
+                         (size_t)2 * kWideRows * sizeof(int32_t);
       static const hipError_t attrw = hipFuncSetAttribute(
           reinterpret_cast<const void*>(cand_vectors_wide_kernel),
           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
