@@ -299,6 +299,7 @@ constexpr int kHalfChunks = 32; // 16-byte chunks per half row (256 bf16)
 constexpr int kHalfStride = kHalfChunks * 16 + 16;  // bytes per half row in LDS (padded)
 constexpr size_t kWideHalfBytes = (size_t)kWideRows * kHalfStride;
 constexpr int kStageRows = 32;                  // output rows per wave per staging round
+constexpr int kNonTemporal = 2;                 // cache-policy bits of a non-temporal store
 constexpr int kStageStride = kWideNb * 16 + 4;  // floats per staged output row (padded)
 static_assert((size_t)kWideWaves * kStageRows * kStageStride * sizeof(float) <= kWideHalfBytes,
               "the output staging fits in LDS half 1");
@@ -498,6 +499,10 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
 
     float* out = side == 0 ? in_vec : out_vec;
     const int64_t row0 = (t >> 1) * ROWS;
+    // the tile's output rows through a buffer descriptor bounded to the rows that exist, so a
+    // store needs one 32-bit offset add and rows past M are dropped by the range check
+    const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
+        out + row0 * d, (short)0, (int)((M - row0) * d * (int64_t)sizeof(float)), 0x00020000);
     // the lane's row and column group, recomputed here (through an empty asm) rather than kept
     // in registers from the top of the kernel: a value reloaded from scratch between the stores
     // would make each 16-row block wait for the previous block's stores to complete
@@ -524,15 +529,18 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
           *reinterpret_cast<f32x4*>(stage + (m2 * 16 + er) * kStageStride + nb * 16 + eg * 4) =
               acc[mb][nb] * inv;
       }
+      // lane: row 2 q + le / 32 of the round, columns col .. col + 3 (past d: outside the range)
+      const int col = col_w + (le & 31) * 4;
+      const uint32_t lane_off =
+          col < d ? (uint32_t)(((le >> 5) * d + col) * (int)sizeof(float)) : 0x80000000u;
 #pragma unroll
       for (int q = 0; q < kStageRows / 2; ++q) {
         const int sr = 2 * q + (le >> 5);
-        const int64_t r = row0 + rnd * kStageRows + sr;
-        const int col = col_w + (le & 31) * 4;
         const f32x4 v =
             *reinterpret_cast<const f32x4*>(stage + sr * kStageStride + (le & 31) * 4);
-        if (r < M && col < d)
-          __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(&out[r * d + col]));
+        const uint32_t row_off = (uint32_t)((rnd * kStageRows + 2 * q) * d * (int)sizeof(float));
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), orsrc,
+                                               lane_off + row_off, 0, kNonTemporal);
       }
     }
     // every wave has read its staged rows back before the next tile's copies go into half 1
@@ -683,7 +691,7 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
     // many 128-row tiles at 448 < d <= 512: the wide persistent kernel
     if (g.dkp == kWideDkp && g.nbp == kWideWaves * kWideNb && ncu > 0 &&
         2 * ((M + kWideRows - 1) / kWideRows) >= 4 * (int64_t)ncu &&
-        V * d * 2 < ((int64_t)1 << 31)) {
+        V * d * 2 < ((int64_t)1 << 31) && M * d * 4 < ((int64_t)1 << 31)) {
       const int64_t wt = 2 * ((M + kWideRows - 1) / kWideRows);
       const int grid = (int)(wt < ncu ? wt : ncu);
       const size_t lds = 2 * kWideHalfBytes + (size_t)kWideWaves * kWideRows * sizeof(float) +
