@@ -344,13 +344,15 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
             wave = (int)__builtin_amdgcn_readfirstlane((uint32_t)(tid / kWave));
   unsigned char* A = smem;                                                // [2][ROWS][32][16 B]
   float* ssbuf = reinterpret_cast<float*>(smem + 2 * kWideHalfBytes);    // [NW][ROWS]
-  int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + NW * ROWS);          // [2][ROWS]
+  int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + NW * ROWS);          // [3][ROWS]
   const size_t slice = (size_t)nbp * 1024;
   const int64_t step = gridDim.x;
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(E), (short)0, (int)(V * d * 2), 0x00020000);
   const uint32_t kOut = 0x80000000u;
   const int dchunks = d / 8;
+  const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(ids), (short)0, (int)(M * (int64_t)sizeof(int32_t)), 0x00020000);
   const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<unsigned char*>(frags), (short)0, (int)(2 * kWideDkp * 3 * slice), 0x00020000);  // 16-byte chunks per embedding row (d % 16 == 0)
 
@@ -372,8 +374,9 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     __asm__ volatile("" : "+s"(row));
     if (lane < kHalfChunks) {
       const int c = h * kHalfChunks + lane;
-      const uint32_t off =
-          (id >= 0 && c < dchunks) ? (uint32_t)id * (uint32_t)(d * 2) + (uint32_t)c * 16u : kOut;
+      const uint32_t off = ((uint32_t)id < (uint32_t)V && c < dchunks)
+                               ? (uint32_t)id * (uint32_t)(d * 2) + (uint32_t)c * 16u
+                               : kOut;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rsrc, (lds_ptr_t)(A + h * kWideHalfBytes + (size_t)row * kHalfStride), 16, off, 0, 0, 0);
     }
@@ -397,19 +400,29 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
   __syncthreads();
 
   for (int it = 0; t < ntiles; ++it, t += step) {
-    const int cur = it & 1, nxt = cur ^ 1;
+    // ids in LDS: slot it % 3 this tile's, (it + 1) % 3 the next tile's (both read just below)
+    const int cur = it % 3, nxt = cur == 2 ? 0 : cur + 1, after = nxt == 2 ? 0 : nxt + 1;
     const bool has_next = t + step < ntiles;
     const int32_t* rc = rid + cur * ROWS;
     const int32_t* rn = rid + nxt * ROWS;
     const int side = (int)(t & 1);
     const uint32_t sbase = (uint32_t)(side * kWideDkp * 3) * (uint32_t)slice;
     const uint32_t voff = (uint32_t)(wave * kWideNb * 1024 + lane * 16);
-    const int32_t id_after = tile_id(t + 2 * step);  // written to rid[cur] at the end
     // ids of the rows this wave copies, lane j holding row wave + 4 j (j < 32): this tile's (for
     // its second half) and the next tile's (for its first half), read once so that a copy needs
     // no LDS read in the k-loop
     const int32_t idc = rc[(wave + NW * (lane & 31)) & (ROWS - 1)];
     const int32_t idn = rn[(wave + NW * (lane & 31)) & (ROWS - 1)];
+    // the ids of the tile after the next are copied by the first two waves straight into slot
+    // (it + 2) % 3 (read by no one during this tile), so no wave waits for them here; rows past
+    // M read as id 0 (their outputs are dropped) and ids outside the vocabulary are caught where
+    // a copy is issued. The copy has landed by the waits at this tile's end.
+    if (wave < ROWS / kWave && t + 2 * step < ntiles) {
+      const int64_t row = ((t + 2 * step) >> 1) * ROWS + wave * kWave + lane;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          irs, (lds_ptr_t)(rid + after * ROWS + wave * kWave), 4,
+          row < M ? (uint32_t)row * 4u : kOut, 0, 0, 0);
+    }
 
     f32x4 acc[8][kWideNb];
 #pragma unroll
@@ -492,7 +505,6 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
       for (int nb = 0; nb < kWideNb; ++nb) __asm__ volatile("" : "+a"(acc[mb][nb]));
-    if (tid < ROWS) rid[cur * ROWS + tid] = id_after;
     // the next tile's first half has landed and nobody reads this tile's second half any more
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -695,7 +707,7 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
       const int64_t wt = 2 * ((M + kWideRows - 1) / kWideRows);
       const int grid = (int)(wt < ncu ? wt : ncu);
       const size_t lds = 2 * kWideHalfBytes + (size_t)kWideWaves * kWideRows * sizeof(float) +
-                         (size_t)2 * kWideRows * sizeof(int32_t);
+                         (size_t)3 * kWideRows * sizeof(int32_t);
       static const hipError_t attrw = hipFuncSetAttribute(
           reinterpret_cast<const void*>(cand_vectors_wide_kernel),
           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
