@@ -74,8 +74,9 @@ def test_vectors_persistent_tiles(lib, d, N, B, K):
     """The persistent kernels at 448 < d <= 512, which copy the next tile's rows into LDS while
     the current tile's products run: 40 x 31 x 33 rows give 1280 tiles of 64 rows (a ragged last
     tile of 24), 70 x 31 x 31 rows 1052 tiles of 128 (a ragged last tile of 70). d = 496 and 464
-    leave the end of every row copy outside the row. Ids outside [0, V) give zero vectors; the
-    oracle takes the in-range rows."""
+    leave the end of every row copy outside the row. Ids outside [0, V) give zero vectors, in the
+    first tiles (whose ids are read before the loop) and in late ones (whose ids are copied while
+    an earlier tile runs); the oracle takes the in-range rows."""
     V = 3000
     print(f"vectors persistent d={d} M={N * B * K}", flush=True)
     rng = np.random.default_rng(d + N)
@@ -86,11 +87,11 @@ def test_vectors_persistent_tiles(lib, d, N, B, K):
     ids = rng.integers(0, V, size=(N, B, K)).astype(np.int32)
     M = N * B * K
     flat = ids.reshape(M)
-    flat[0], flat[M - 1], flat[5000], flat[M - 30] = 7, 7, -1, V
+    flat[0], flat[M - 1], flat[5000], flat[M - 30], flat[M - 200] = 7, 7, -1, V, -5
     E = torch.from_numpy(E32).to(torch.bfloat16)
     giv, gov = _gpu_vectors(lib, ids, E, torch.from_numpy(W_in), torch.from_numpy(W_out))
     giv, gov = giv.reshape(M, d), gov.reshape(M, d)
-    for r in (5000, M - 30):
+    for r in (5000, M - 30, M - 200):
         assert (giv[r] == 0).all() and (gov[r] == 0).all(), f"row {r} of an out-of-range id"
     sample = np.unique(np.concatenate([np.arange(64), np.arange(M - 64, M),
                                        rng.choice(M, 700, replace=False)]))
