@@ -85,6 +85,8 @@ EDGE = [
     (2, 16, 151936, 16, "normal"),
     # more than 2048 partial keys per row: the merge kernel's list-merging path
     (1, 1, 300000, 64, "normal"),
+    # the most rows the short-segment path takes (256 rows of two segments)
+    (1, 256, 10000, 4, "normal"),
 ]
 
 
@@ -117,6 +119,25 @@ def test_topk_edge_cases(lib, case, dtype):
     x = _edge_logits(N, B, V, kind, case)
     t = _bf16(x) if dtype == "bf16" else torch.from_numpy(x)
     _check_rows(lib, t, K, None, f"edge{case}-{dtype}")
+
+
+def test_topk_workspace_shared_across_paths(lib):
+    """One zero-filled workspace through short-segment, streaming split and whole-row calls in
+    turn: every call matches the same call on a fresh workspace bit for bit."""
+    shapes = [(1, 16, 151936, 8), (2, 16, 151936, 16), (1, 256, 10000, 4), (4, 16, 151936, 16),
+              (1, 16, 151936, 8), (1, 3, 30000, 12)]
+    need = max(lib.lilicorr_topk_workspace_bytes(N, B, V, K) for N, B, V, K in shapes)
+    ws = torch.zeros((need + 15) // 16 * 16, dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(17)
+    for i, (N, B, V, K) in enumerate(shapes):
+        print(f"topk shared workspace call {i}: N={N} B={B} V={V} K={K}", flush=True)
+        x = _bf16(rng.standard_normal((N, B, V)) * 2).cuda()
+        ids, logp = lib.topk(x, K, workspace=ws)
+        ids0, logp0 = lib.topk(x, K)
+        torch.cuda.synchronize()
+        assert_equal(to_np(ids), to_np(ids0), f"call {i} ids")
+        assert_equal(to_np(logp), to_np(logp0), f"call {i} logp")
+    assert lib.topk_wait_status(ws) == 0
 
 
 def test_topk_sparse_finite_row(lib):
