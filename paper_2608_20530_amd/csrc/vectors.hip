@@ -265,40 +265,40 @@ __global__ __launch_bounds__(512) void cand_vectors_stream_kernel(
 
 // Wide persistent variant for many tiles at 448 < d <= 512 (32 k-blocks of the contraction, 32
 // column blocks). The weight fragments stream from L2 once per tile and are reused by every row
-// of it, so the L2 read per row falls with the tile height; at 64 rows (two waves per SIMD, 256
-// registers each) the fragment read keeps pace with the matrix cores only just. Here a tile is
-// 128 rows and each of four waves (one per SIMD, so 512 registers: the 128 x 128 accumulator
-// block in the accumulation registers) owns 128 columns, which halves the L2 read per row.
+// of it, so the L2 read per row falls with the tile height; at 64 rows the fragment read keeps
+// pace with the matrix cores only just. Here a tile is 128 rows and each of eight waves (two per
+// SIMD, 256 registers each) owns 64 columns: its 128 x 64 accumulator block sits in ordinary
+// registers, where the matrix cores run faster than from the accumulation registers (a
+// register-only probe of this loop shape: 1.98 against 1.1-1.7 PFLOP/s).
 //  * The gathered tile (128 rows of bf16, both halves of the k range) lives in LDS as
 //    [half][row][256 bf16 + 8 of padding], so the 16 rows one fragment read touches fall in 16
 //    different bank groups and every k-block's reads sit at fixed offsets from one lane base.
 //  * Rows arrive by direct global-to-LDS loads, one half row per wave instruction (32 lanes),
-//    four per wave in every k-block: a tile's second half while its first half is multiplied,
-//    the next tile's first half while its second half is. The ids of a wave's 32 rows sit one
+//    two per wave in every k-block: a tile's second half while its first half is multiplied,
+//    the next tile's first half while its second half is. The ids of a wave's 16 rows sit one
 //    per lane, so a copy reads no LDS in the k-loop.
 //  * The k-block loop is unrolled, so the accumulators stay in place across k-blocks, and the
 //    weight fragments come through a buffer descriptor with one lane offset (their k-block and
-//    term displacements are scalar), in pieces of two column blocks with three pieces in flight.
+//    term displacements are scalar), one column block at a time with two in flight.
 //  * Nothing spills: a value reloaded from scratch in the output phase would make each 16-row
 //    block of stores wait for the previous block's to complete.
 //  * The unit vectors go out through LDS half 1, free between the last k-block and the next
-//    tile's first copies into it: each wave stages 32 rows x its 128 columns at a time (four
+//    tile's first copies into it: each wave stages 16 rows x its 64 columns at a time (eight
 //    rounds per tile) and reads them back so that each non-temporal store instruction covers
-//    whole 128-byte lines (two rows x 512 bytes): 16-byte pieces of 16 rows per instruction
-//    wrote 1.5x the bytes to HBM, 8-row rounds through a separate staging area took 1.2 us
-//    more per tile, and ordinary stores left the next
-//    kernel's reads behind the L2's write-backs.
+//    whole 128-byte lines (four rows x 256 bytes): 16-byte pieces of 16 rows per instruction
+//    wrote 1.5x the bytes to HBM, and ordinary stores left the next kernel's reads behind the
+//    L2's write-backs.
 //  * Products run with the weight fragment as the first operand, so each lane ends up holding
 //    four consecutive columns of one row.
 // Tile t is side t % 2 (0: W_in), rows (t / 2) * 128 onwards.
 constexpr int kWideRows = 128;
-constexpr int kWideWaves = 4;
-constexpr int kWideNb = 8;      // 16-column blocks per wave
+constexpr int kWideWaves = 8;
+constexpr int kWideNb = 4;      // 16-column blocks per wave
 constexpr int kWideDkp = 16;    // 32-deep k-blocks
 constexpr int kHalfChunks = 32; // 16-byte chunks per half row (256 bf16)
 constexpr int kHalfStride = kHalfChunks * 16 + 16;  // bytes per half row in LDS (padded)
 constexpr size_t kWideHalfBytes = (size_t)kWideRows * kHalfStride;
-constexpr int kStageRows = 32;                  // output rows per wave per staging round
+constexpr int kStageRows = 16;                  // output rows per wave per staging round
 constexpr int kNonTemporal = 2;                 // cache-policy bits of a non-temporal store
 constexpr int kStageStride = kWideNb * 16 + 4;  // floats per staged output row (padded)
 static_assert((size_t)kWideWaves * kStageRows * kStageStride * sizeof(float) <= kWideHalfBytes,
@@ -333,7 +333,7 @@ __device__ __forceinline__ void wide_mfma(f32x4 (&acc)[8][kWideNb], const BFrag<
             __builtin_bit_cast(bf16x8, b[j][t]), a[mb], acc[mb][NBP * g + j], 0, 0, 0);
 }
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* __restrict__ E,
                               const unsigned char* __restrict__ frags, int64_t M, int64_t V,
                               int d, int nbp, int64_t ntiles, float* __restrict__ in_vec,
@@ -408,11 +408,11 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     const int side = (int)(t & 1);
     const uint32_t sbase = (uint32_t)(side * kWideDkp * 3) * (uint32_t)slice;
     const uint32_t voff = (uint32_t)(wave * kWideNb * 1024 + lane * 16);
-    // ids of the rows this wave copies, lane j holding row wave + 4 j (j < 32): this tile's (for
+    // ids of the rows this wave copies, lane j holding row wave + 8 j (j < 16): this tile's (for
     // its second half) and the next tile's (for its first half), read once so that a copy needs
     // no LDS read in the k-loop
-    const int32_t idc = rc[(wave + NW * (lane & 31)) & (ROWS - 1)];
-    const int32_t idn = rn[(wave + NW * (lane & 31)) & (ROWS - 1)];
+    const int32_t idc = rc[(wave + NW * (lane & (ROWS / NW - 1))) & (ROWS - 1)];
+    const int32_t idn = rn[(wave + NW * (lane & (ROWS / NW - 1))) & (ROWS - 1)];
     // the ids of the tile after the next are copied by the first two waves straight into slot
     // (it + 2) % 3 (read by no one during this tile), so no wave waits for them here; rows past
     // M read as id 0 (their outputs are dropped) and ids outside the vocabulary are caught where
@@ -431,7 +431,7 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
       for (int nb = 0; nb < kWideNb; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     // the weight fragments of a k-block come in pieces of kPieceNb column blocks through
     // kBufs register buffers: while a piece is multiplied the next kBufs - 1 are in flight
-    constexpr int kPieceNb = 2, kPieces = kWideNb / kPieceNb, kBufs = 4;
+    constexpr int kPieceNb = 1, kPieces = kWideNb / kPieceNb, kBufs = 3;
     constexpr int kTotalPieces = kWideDkp * kPieces;
     BFrag<kPieceNb> bq[kBufs];
     auto load_piece = [&](int p) {
@@ -441,7 +441,7 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
 #pragma unroll
     for (int p = 0; p < kBufs - 1; ++p) load_piece(p);
     const int arow = lane & 15, agrp = lane >> 4;
-    // k-blocks kb0 .. kb0+7 from LDS half h. Four half-row copies per k-block go into the other
+    // k-blocks kb0 .. kb0+7 from LDS half h. Two half-row copies per k-block go into the other
     // half: this tile's second half while the first is multiplied (that half was released at
     // the previous tile's end), the next tile's first half while the second is multiplied.
     auto kloop = [&](int kb0, int h) {
@@ -449,16 +449,17 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
 #pragma unroll
       for (int kb = kb0; kb < kb0 + 8; ++kb) {
         __builtin_amdgcn_sched_barrier(0);
+        constexpr int kCopies = ROWS / NW / 8;  // half-row copies per wave per k-block
         if (h == 0) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int j = 4 * (kb - kb0) + i;
+          for (int i = 0; i < kCopies; ++i) {
+            const int j = kCopies * (kb - kb0) + i;
             dma_half_id(__builtin_amdgcn_readlane(idc, j), 1, wave + NW * j);
           }
         } else if (has_next) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int j = 4 * (kb - kb0) + i;
+          for (int i = 0; i < kCopies; ++i) {
+            const int j = kCopies * (kb - kb0) + i;
             dma_half_id(__builtin_amdgcn_readlane(idn, j), 0, wave + NW * j);
           }
         }
@@ -486,7 +487,7 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     __syncthreads();
     kloop(8, 1);
 
-    // this wave's 128-column part of every row's squared norm: lane l holds row 16 mb + l % 16,
+    // this wave's 64-column part of every row's squared norm: lane l holds row 16 mb + l % 16,
     // columns 16 nb + 4 (l / 16) + i
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
@@ -499,12 +500,6 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
       s += __shfl_xor(s, 32, kWave);
       if (lane < 16) ssbuf[wave * ROWS + mb * 16 + lane] = s;
     }
-    // keep the accumulators in the accumulation registers between the two passes over them
-    // (copied into ordinary registers, they crowd out everything else and force spills)
-#pragma unroll
-    for (int mb = 0; mb < 8; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < kWideNb; ++nb) __asm__ volatile("" : "+a"(acc[mb][nb]));
     // the next tile's first half has landed and nobody reads this tile's second half any more
     __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -522,8 +517,8 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     __asm__ volatile("" : "+v"(le));
     const int er = le & 15, eg = le >> 4;
     // the output leaves through LDS half 1 (free until the next tile's copies into it begin):
-    // each wave stages kStageRows rows x its 128 columns at a time, read back so that each half
-    // wave writes 512 contiguous bytes (whole lines) of one row with non-temporal stores
+    // each wave stages kStageRows rows x its 64 columns at a time, read back so that each 16
+    // lanes write 256 contiguous bytes (whole lines) of one row with non-temporal stores
     float* stage = reinterpret_cast<float*>(A + kWideHalfBytes) + wave * kStageRows * kStageStride;
     const int col_w = wave * kWideNb * 16;
 #pragma unroll
@@ -541,16 +536,16 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
           *reinterpret_cast<f32x4*>(stage + (m2 * 16 + er) * kStageStride + nb * 16 + eg * 4) =
               acc[mb][nb] * inv;
       }
-      // lane: row 2 q + le / 32 of the round, columns col .. col + 3 (past d: outside the range)
-      const int col = col_w + (le & 31) * 4;
+      // lane: row 4 q + le / 16 of the round, columns col .. col + 3 (past d: outside the range)
+      const int col = col_w + (le & 15) * 4;
       const uint32_t lane_off =
-          col < d ? (uint32_t)(((le >> 5) * d + col) * (int)sizeof(float)) : 0x80000000u;
+          col < d ? (uint32_t)(((le >> 4) * d + col) * (int)sizeof(float)) : 0x80000000u;
 #pragma unroll
-      for (int q = 0; q < kStageRows / 2; ++q) {
-        const int sr = 2 * q + (le >> 5);
+      for (int q = 0; q < kStageRows / 4; ++q) {
+        const int sr = 4 * q + (le >> 4);
         const f32x4 v =
-            *reinterpret_cast<const f32x4*>(stage + sr * kStageStride + (le & 31) * 4);
-        const uint32_t row_off = (uint32_t)((rnd * kStageRows + 2 * q) * d * (int)sizeof(float));
+            *reinterpret_cast<const f32x4*>(stage + sr * kStageStride + (le & 15) * 4);
+        const uint32_t row_off = (uint32_t)((rnd * kStageRows + 4 * q) * d * (int)sizeof(float));
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), orsrc,
                                                lane_off + row_off, 0, kNonTemporal);
       }
