@@ -448,6 +448,15 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
       const unsigned char* Ah = A + h * kWideHalfBytes;
 #pragma unroll
       for (int kb = kb0; kb < kb0 + 8; ++kb) {
+        // the two waves of a SIMD take turns by progress: a wave lowers its issue priority as it
+        // moves through the k-blocks, so the one behind is served first and both reach the
+        // barrier together
+        if ((kb & 3) == 0) {
+          if (kb == 0) __builtin_amdgcn_s_setprio(3);
+          else if (kb == 4) __builtin_amdgcn_s_setprio(2);
+          else if (kb == 8) __builtin_amdgcn_s_setprio(1);
+          else __builtin_amdgcn_s_setprio(0);
+        }
         __builtin_amdgcn_sched_barrier(0);
         constexpr int kCopies = ROWS / NW / 8;  // half-row copies per wave per k-block
         if (h == 0) {
