@@ -38,11 +38,11 @@ struct VecGeom {
   int rm;     // 16-row blocks per workgroup of the candidate-vector kernel
 };
 
-// rm: up to d = 256, 128-row tiles once there are enough of them to give every compute unit
-// several (a workgroup's phases, gather -> MFMA -> store, then overlap with other workgroups'),
-// else 64-row tiles, which put two workgroups on each compute unit; 64-row tiles for
-// 256 < d <= 512 (a 128-row tile there needs 133 KB of LDS, one workgroup per compute unit, and
-// measured 7% slower at 131072 rows, d = 512); 32-row tiles above d = 512
+// rm: 64-row tiles up to d = 512 (two workgroups per compute unit; at d <= 256 a 128-row tile's
+// 8 x 4 accumulator blocks plus two weight buffers exceed the 256 registers of two waves per
+// SIMD and spilled: 175 against 160 us at 131072 rows, d = 256; at 256 < d <= 512 it needs 133 KB
+// of LDS, one workgroup per compute unit, and measured 7% slower at 131072 rows, d = 512);
+// 32-row tiles above d = 512. (Many tiles at 448 < d <= 512 take the persistent kernels.)
 inline VecGeom vec_geom(int d, int64_t M = 0) {
   VecGeom g;
   g.d16 = d / 16;
@@ -50,7 +50,8 @@ inline VecGeom vec_geom(int d, int64_t M = 0) {
   g.dk = (d + 31) / 32;
   g.dkp = (g.dk + 1) / 2 * 2;
   g.waves = g.nbp / kNbPerWave;
-  g.rm = d > 512 ? 2 : (d > 256 ? 4 : ((M + 127) / 128 * 2 >= 2048 ? 8 : 4));
+  (void)M;
+  g.rm = d > 512 ? 2 : 4;
   return g;
 }
 
@@ -124,6 +125,54 @@ __device__ __forceinline__ void project_tile(f32x4 (&acc)[RM][NB], BFrag<NB>& b0
     __builtin_amdgcn_sched_barrier(0);
     mfma_kblock<RM, NB>(acc, b1, A, astride, kb + 1, lane);
     __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// The same contraction with the weight fragments one column block at a time through four
+// register buffers (three in flight): 48 registers of weights instead of 96, for a kernel held to
+// 128 registers (1024-thread workgroups). Buffer p % 4 of piece p = (k-block, column block) is the
+// column block itself, so the ring index is fixed at compile time; each accumulator sees the same
+// sequence of MFMAs as in project_tile, so the results are identical.
+template <int RM>
+__device__ __forceinline__ void project_tile_lean(f32x4 (&acc)[RM][kNbPerWave], const uint16_t* A,
+                                                  int astride, const unsigned char* wf,
+                                                  size_t slice, int dkp, int lane) {
+  constexpr int NB = kNbPerWave;
+  static_assert(NB == 4, "one register buffer per column block");
+#pragma unroll
+  for (int mb = 0; mb < RM; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4 bq[NB][3];
+  auto load = [&](int kb, int nb) {
+    const unsigned char* q = wf + (size_t)kb * 3 * slice + nb * 1024;
+#pragma unroll
+    for (int t = 0; t < 3; ++t) bq[nb][t] = *reinterpret_cast<const u32x4*>(q + t * slice);
+  };
+  load(0, 0);
+  load(0, 1);
+  load(0, 2);
+  for (int kb = 0; kb < dkp; ++kb) {
+    bf16x8 a[RM];
+    const int kcol = kb * 32 + (lane >> 4) * 8;
+#pragma unroll
+    for (int mb = 0; mb < RM; ++mb)
+      a[mb] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(A + (mb * 16 + (lane & 15)) * astride + kcol));
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      // piece 4 kb + nb + 3: column block nb + 3 of this k-block, or nb - 1 of the next
+      if (nb == 0) load(kb, 3);
+      else if (kb + 1 < dkp) load(kb + 1, nb - 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int mb = 0; mb < RM; ++mb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              a[mb], __builtin_bit_cast(bf16x8, bq[nb][t]), acc[mb][nb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 }
 

@@ -108,7 +108,12 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   __syncthreads();
 
   f32x4 acc[RM][kNbPerWave];
-  project_tile<RM, kNbPerWave>(acc, b0, A, astride, wf, slice, dkp, lane);
+  if constexpr (MAXT > 512) {
+    (void)b0;  // the 1024-thread instance streams its weights one column block at a time
+    project_tile_lean<RM>(acc, A, astride, wf, slice, dkp, lane);
+  } else {
+    project_tile<RM, kNbPerWave>(acc, b0, A, astride, wf, slice, dkp, lane);
+  }
   row_sumsq<RM, kNbPerWave>(acc, ssbuf + wave * ROWS, lane);
   __syncthreads();
   float* out = side == 0 ? in_vec : out_vec;
@@ -735,14 +740,7 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
                        (size_t)g.waves * rows_wg * sizeof(float) + (size_t)rows_wg * sizeof(int32_t);
     const dim3 grid((unsigned)nblk, 2), block(g.waves * kWave);
     const uint16_t* e16 = static_cast<const uint16_t*>(E);
-    if (g.rm == 8) {
-      static const hipError_t attr8 = hipFuncSetAttribute(
-          reinterpret_cast<const void*>(cand_vectors_mfma_kernel<8, 512>),
-          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      (void)attr8;
-      hipLaunchKernelGGL((cand_vectors_mfma_kernel<8, 512>), grid, block, lds, stream, ids, e16, p,
-                         M, V, d, g.nbp, g.dkp, in_vec, out_vec);
-    } else if (g.rm == 4) {
+    if (g.rm == 4) {
       static const hipError_t attr4 = hipFuncSetAttribute(
           reinterpret_cast<const void*>(cand_vectors_mfma_kernel<4, 512>),
           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
