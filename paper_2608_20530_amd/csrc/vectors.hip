@@ -137,136 +137,7 @@ __global__ __launch_bounds__(MAXT) void cand_vectors_mfma_kernel(
   }
 }
 
-// Persistent variant for many tiles at 480 < d <= 512, d a multiple of 8 (a gathered row is at
-// most 1 KB of bf16: one wave-wide load of 16 aligned bytes per lane). Registers allow one 64-row workgroup per compute unit there,
-// so in the plain kernel each tile's gather and output phases leave the matrix cores idle. Here
-// one workgroup per compute unit takes tiles t, t + grid, ... and keeps two LDS tiles: while the
-// MFMA loop runs on one, the next tile's rows are copied into the other by direct global-to-LDS
-// loads (no registers), two rows per wave in each of the loop's first four trips, so they have
-// landed, behind the weight-fragment loads the loop waits for anyway, long before the tile ends.
-// Tile t is side t % 2 (0: W_in), rows (t / 2) * 64 onwards; the ids two tiles ahead are read
-// during the current tile.
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
-constexpr int kStreamDkp = 16;  // 32-deep k-blocks of the contraction (d <= 512, DPAD = 512)
-
-__global__ __launch_bounds__(512) void cand_vectors_stream_kernel(
-    const int32_t* __restrict__ ids, const uint16_t* __restrict__ E,
-    const unsigned char* __restrict__ frags, int64_t M, int64_t V, int d, int nbp,
-    int64_t ntiles, float* __restrict__ in_vec, float* __restrict__ out_vec) {
-  constexpr int RM = 4, ROWS = RM * 16, DKP = kStreamDkp, TRIPS = DKP / 2;
-  constexpr int DPAD = DKP * 32, ASTRIDE = DPAD + 8;
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int nthreads = blockDim.x, nwaves = nthreads / kWave;  // nwaves = 8: 8 rows per wave
-  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  uint16_t* A0 = reinterpret_cast<uint16_t*>(smem);                      // [2][ROWS][ASTRIDE]
-  float* ssbuf = reinterpret_cast<float*>(A0 + 2 * ROWS * ASTRIDE);       // [2][nwaves][ROWS]
-  int32_t* rid = reinterpret_cast<int32_t*>(ssbuf + 2 * nwaves * ROWS);  // [2][ROWS]
-  const size_t slice = (size_t)nbp * 1024;
-  const int64_t step = gridDim.x;
-  // rows of E as one buffer: a lane past the row's d columns, or a zero row, reads out of range
-  // and the load writes zeros into LDS
-  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(E), (short)0, (int)(V * d * 2), 0x00020000);
-  const uint32_t kOut = 0x80000000u;
-
-  // ids of tile t's rows (-1: a zero row), one per thread tid < ROWS
-  auto tile_id = [&](int64_t t) -> int32_t {
-    int32_t v = -1;
-    if (t < ntiles && tid < ROWS) {
-      const int64_t row = (t >> 1) * ROWS + tid;
-      if (row < M) {
-        const int32_t id = ids[row];
-        v = (id >= 0 && id < V) ? id : -1;
-      }
-    }
-    return v;
-  };
-
-  int64_t t = blockIdx.x;
-  {
-    const int32_t v0 = tile_id(t), v1 = tile_id(t + step);
-    if (tid < ROWS) {
-      rid[tid] = v0;
-      rid[ROWS + tid] = v1;
-    }
-  }
-  __syncthreads();
-  gather_rows(A0, ASTRIDE, ROWS, rid, E, d, DPAD, tid, nthreads);
-  __syncthreads();
-
-  for (int it = 0; t < ntiles; ++it, t += step) {
-    const int cur = it & 1, nxt = cur ^ 1;
-    const bool has_next = t + step < ntiles;
-    const uint16_t* Ac = A0 + cur * ROWS * ASTRIDE;
-    uint16_t* An = A0 + nxt * ROWS * ASTRIDE;
-    const int32_t* rn = rid + nxt * ROWS;
-    const int side = (int)(t & 1);
-    const unsigned char* wf =
-        frags + (size_t)side * DKP * 3 * slice + (size_t)wave * kNbPerWave * 1024 + lane * 16;
-    // row r of the next tile into LDS (every lane of the wave, r wave-uniform)
-    auto dma_row = [&](int r) {
-      const int32_t id = __builtin_amdgcn_readfirstlane(rn[r]);
-      const uint32_t off = (id >= 0 && lane * 8 < d)
-                               ? (uint32_t)id * (uint32_t)(d * 2) + (uint32_t)lane * 16u
-                               : kOut;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_ptr_t)(An + r * ASTRIDE), 16, off, 0,
-                                               0, 0);
-    };
-
-    f32x4 acc[RM][kNbPerWave];
-#pragma unroll
-    for (int mb = 0; mb < RM; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < kNbPerWave; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    BFrag<kNbPerWave> b0, b1;
-    load_bfrag<kNbPerWave>(b0, wf, slice, 0);
-    const int32_t id_after = tile_id(t + 2 * step);  // written to rid[cur] at the end
-#pragma unroll 1
-    for (int tr = 0; tr < TRIPS; ++tr) {
-      load_bfrag<kNbPerWave>(b1, wf, slice, 2 * tr + 1);
-      // wave w copies rows w, w + nwaves, ..., two per trip over the first four trips
-      if (has_next && tr < 4) {
-        dma_row(wave + nwaves * (2 * tr));
-        dma_row(wave + nwaves * (2 * tr + 1));
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_kblock<RM, kNbPerWave>(acc, b0, Ac, ASTRIDE, 2 * tr, lane);
-      __builtin_amdgcn_sched_barrier(0);
-      load_bfrag<kNbPerWave>(b0, wf, slice, 2 * tr + 2 < DKP ? 2 * tr + 2 : DKP - 1);
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_kblock<RM, kNbPerWave>(acc, b1, Ac, ASTRIDE, 2 * tr + 1, lane);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    row_sumsq<RM, kNbPerWave>(acc, ssbuf + (cur * nwaves + wave) * ROWS, lane);
-    if (tid < ROWS) rid[cur * ROWS + tid] = id_after;
-    // this wave's copies have landed; then the barrier: the next tile is complete in LDS, the
-    // norms are in, and nobody reads this tile's LDS any more
-    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-
-    const float* ss = ssbuf + cur * nwaves * ROWS;
-    float* out = side == 0 ? in_vec : out_vec;
-    const int64_t row0 = (t >> 1) * ROWS;
-    const int col0 = wave * kNbPerWave * 16 + (lane & 15);
-#pragma unroll
-    for (int mb = 0; mb < RM; ++mb) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int rl = mb * 16 + (lane >> 4) * 4 + i;
-        float tot = 0.f;
-        for (int g = 0; g < nwaves; ++g) tot += ss[g * ROWS + rl];
-        const float inv = tot > 0.f ? 1.0f / sqrtf(tot) : 0.f;
-        const int64_t r = row0 + rl;
-        if (r < M) {
-#pragma unroll
-          for (int nb = 0; nb < kNbPerWave; ++nb)
-            if (col0 + nb * 16 < d)
-              __builtin_nontemporal_store(acc[mb][nb][i] * inv, &out[r * d + col0 + nb * 16]);
-        }
-      }
-    }
-  }
-}
 
 // Wide persistent variant for many tiles at 448 < d <= 512 (32 k-blocks of the contraction, 32
 // column blocks). The weight fragments stream from L2 once per tile and are reused by every row
@@ -521,9 +392,12 @@ void cand_vectors_wide_kernel(const int32_t* __restrict__ ids, const uint16_t* _
     float* out = side == 0 ? in_vec : out_vec;
     const int64_t row0 = (t >> 1) * ROWS;
     // the tile's output rows through a buffer descriptor bounded to the rows that exist, so a
-    // store needs one 32-bit offset add and rows past M are dropped by the range check
+    // store needs one 32-bit offset add and rows past M are dropped by the range check (the
+    // 64-bit base moves with the tile, so only the tile's own 256 KB need 32-bit offsets)
+    const int64_t out_bytes = (M - row0) * d * (int64_t)sizeof(float);
     const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
-        out + row0 * d, (short)0, (int)((M - row0) * d * (int64_t)sizeof(float)), 0x00020000);
+        out + row0 * d, (short)0, (int)(out_bytes < 0x7fffffff ? out_bytes : 0x7fffffff),
+        0x00020000);
     // the lane's row and column group, recomputed here (through an empty asm) rather than kept
     // in registers from the top of the kernel: a value reloaded from scratch between the stores
     // would make each 16-row block wait for the previous block's stores to complete
@@ -581,20 +455,6 @@ int compute_units() {
     cached[dev] = n;
   }
   return cached[dev];
-}
-
-void launch_stream(int64_t ntiles, int grid, int waves, const int32_t* ids, const uint16_t* E,
-                   const unsigned char* frags, int64_t M, int64_t V, int d, int nbp, float* in_vec,
-                   float* out_vec, hipStream_t stream) {
-  constexpr int ROWS = 64, ASTRIDE = kStreamDkp * 32 + 8;
-  const size_t lds = (size_t)2 * ROWS * ASTRIDE * 2 + (size_t)2 * waves * ROWS * sizeof(float) +
-                     (size_t)2 * ROWS * sizeof(int32_t);
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(cand_vectors_stream_kernel),
-      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-  (void)attr;
-  hipLaunchKernelGGL(cand_vectors_stream_kernel, dim3((unsigned)grid), dim3(waves * kWave), lds,
-                     stream, ids, E, frags, M, V, d, nbp, ntiles, in_vec, out_vec);
 }
 
 constexpr int kF32Rows = 16;
@@ -709,10 +569,11 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
     const int64_t nblk = (M + rows_wg - 1) / rows_wg;
     if (nblk > 0x7fffffffll) return LILICORR_ERR_UNSUPPORTED;
     const int ncu = compute_units();
-    // many 128-row tiles at 448 < d <= 512: the wide persistent kernel
+    // at 448 < d <= 512, from one 128-row tile per compute unit: the wide persistent kernel (E
+    // and the ids addressable by 32-bit buffer offsets)
     if (g.dkp == kWideDkp && g.nbp == kWideWaves * kWideNb && ncu > 0 &&
-        2 * ((M + kWideRows - 1) / kWideRows) >= 4 * (int64_t)ncu &&
-        V * d * 2 < ((int64_t)1 << 31) && M * d * 4 < ((int64_t)1 << 31)) {
+        2 * ((M + kWideRows - 1) / kWideRows) >= (int64_t)ncu &&
+        V * d * 2 < ((int64_t)1 << 31) && M * 4 < ((int64_t)1 << 31)) {
       const int64_t wt = 2 * ((M + kWideRows - 1) / kWideRows);
       const int grid = (int)(wt < ncu ? wt : ncu);
       const size_t lds = 2 * kWideHalfBytes + (size_t)kWideWaves * kWideRows * sizeof(float) +
@@ -724,16 +585,6 @@ extern "C" lilicorr_status lilicorr_candidate_vectors(const int32_t* ids, const 
       hipLaunchKernelGGL(cand_vectors_wide_kernel, dim3((unsigned)grid), dim3(kWideWaves * kWave),
                          lds, stream, ids, static_cast<const uint16_t*>(E), p, M, V, d, g.nbp, wt,
                          in_vec, out_vec);
-      return launch_status();
-    }
-    // many 64-row tiles at 480 < d <= 512: the persistent kernel (at least four tiles per
-    // compute unit; E addressable by a 32-bit buffer offset)
-    const int64_t ntiles = 2 * nblk;
-    if (g.rm == 4 && g.dkp == kStreamDkp && g.waves == 8 && d % 8 == 0 && ncu > 0 &&
-        ntiles >= 4 * (int64_t)ncu && V * d * 2 < ((int64_t)1 << 31)) {
-      const int grid = (int)(ntiles < ncu ? ntiles : ncu);
-      launch_stream(ntiles, grid, g.waves, ids, static_cast<const uint16_t*>(E), p, M, V, d, g.nbp,
-                    in_vec, out_vec, stream);
       return launch_status();
     }
     const size_t lds = (size_t)rows_wg * (g.dkp * 32 + 8) * 2 +

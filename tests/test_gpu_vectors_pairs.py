@@ -69,13 +69,15 @@ def test_vectors_shapes(lib, d, K, N, B, e_dtype):
 
 
 @pytest.mark.parametrize("d,N,B,K", [(512, 40, 31, 33), (496, 40, 31, 33),
-                                     (512, 70, 31, 31), (464, 70, 31, 31), (512, 64, 32, 32)])
+                                     (512, 70, 31, 31), (464, 70, 31, 31), (512, 64, 32, 32),
+                                     (512, 16, 32, 32)])
 def test_vectors_persistent_tiles(lib, d, N, B, K):
-    """The persistent kernels at 448 < d <= 512, which copy the next tile's rows into LDS while
-    the current tile's products run: 40 x 31 x 33 rows give 1280 tiles of 64 rows (a ragged last
-    tile of 24), 70 x 31 x 31 rows 1052 tiles of 128 (a ragged last tile of 70), 64 x 32 x 32
-    rows exactly 1024 tiles of 128 (four per compute unit, no ragged tile). d = 496 and 464
-    leave the end of every row copy outside the row. Ids outside [0, V) give zero vectors, in the
+    """The persistent kernel at 448 < d <= 512, which copies the next tile's rows into LDS while
+    the current tile's products run (128-row tiles, each side a tile of its own): 40 x 31 x 33
+    rows give 640 tiles (a ragged last tile of 88 rows), 70 x 31 x 31 rows 1052 (a ragged last
+    tile of 70), 64 x 32 x 32 rows exactly 1024 (four per compute unit) and 16 x 32 x 32 rows 256
+    (one per compute unit, the fewest that take this kernel). d = 496 and 464 leave the end of
+    every row copy outside the row. Ids outside [0, V) give zero vectors, in the
     first tiles (whose ids are read before the loop) and in late ones (whose ids are copied while
     an earlier tile runs); the oracle takes the in-range rows."""
     V = 3000
